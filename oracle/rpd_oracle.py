@@ -1,0 +1,332 @@
+"""fp64 reference of the Reliable Parallel Decoding (RPD) commit step.
+
+TEST INFRASTRUCTURE ONLY. This module is the plain, slow, obviously correct
+CPU statement of what the commit step computes. Only the test suite, the
+package smoke check and the CPU-baseline leg of the benchmark may import it;
+the product path never does, and it shares no code with the HIP library.
+
+Every function follows a passage of the paper (He, Liu, Xiong, Zhang,
+"Reliable Parallel Decoding in Masked Diffusion Language Models"):
+
+* projection of hidden states through the unembedding ("logit lens") --
+  Section 2.2 and Appendix A.2 "Intermediate-layer readout", Appendix A.6
+  "Layerwise projection";
+* entropy ``H(p) = -sum_v p(v) log p(v)`` in nats -- Eq. (1), Section 2.1;
+* prediction persistence ``K_i`` -- Eq. (2), Section 2.2 and Appendix A.2;
+* confidence drop ``r_i`` -- Eq. (3), Section 2.2 and Appendix A.2;
+* stability score ``S_i = min(K_i, K_max) - w r_i`` -- Eq. (4), Section 3.1;
+* candidate set -- Eq. (5), Section 3.1;
+* sequential cumulative-entropy commitment and the progress fallback --
+  Section 3.2 (definitions of ``E_i`` and ``A_t``), hyperparameters in
+  Table 4 (Appendix A.6).
+
+Readings where the paper is silent (stated once here, used throughout):
+the supplied hidden states are already normalised (the projection is a plain
+product with W_U); the scoring softmax uses temperature 1; argmax ties go to
+the lowest vocabulary index; the layer window is the K layers supplied, with
+layer K-1 the final one; ``p^(l)(y_i)`` in the drop is the probability of the
+final-layer token; sequences of a batch are independent; "the first W masked
+positions" are the first W entries of the masked list in canvas order; the
+fallback ignores NaN confidences and picks the lowest index among equals.
+
+Arithmetic is float64 on the exact values of the bf16 / fp32 inputs.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+# flag bits of the per-position record (same meaning on every side)
+FLAG_CANDIDATE = 1
+FLAG_HIGH_CONF = 2
+FLAG_STABLE = 4
+FLAG_COMMITTED = 8
+FLAG_FALLBACK = 16
+
+
+@dataclass(frozen=True)
+class Params:
+    """Hyperparameters of the commit rule (Table 4, Appendix A.6)."""
+    theta_h: float = 0.9     # high-confidence threshold, bypasses stability
+    theta_c: float = 0.6     # minimum confidence for stability admission
+    theta_s: float = 3.5     # stability threshold
+    w: float = 15.0          # weight of the confidence-drop penalty
+    k_max: int = 6           # cap on persistence
+    beta: float = 4.0        # cumulative entropy budget, nats
+    window: int = 32         # fallback window W
+
+
+LLADA = Params(theta_s=3.5, w=15.0)
+DREAM = Params(theta_s=2.5, w=20.0)
+
+
+def strict(K: int, beta: float = 1.0) -> Params:
+    """The rule "argmax agrees across all K layers and its probability does
+    not drop at the final layer" expressed in Eq. (4): with w = 1, K_max >= K
+    and theta_s = K, S_i >= theta_s holds exactly when K_i = K and r_i = 0."""
+    return Params(theta_h=0.9, theta_c=0.6, theta_s=float(K), w=1.0,
+                  k_max=max(K, 6), beta=beta, window=32)
+
+
+# ------------------------------------------------------------- inputs ----
+
+def to_f64(a: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact float64 values of bf16 bit patterns (uint16) or fp32 values."""
+    if dtype == "bf16":
+        return (np.asarray(a).astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    if dtype == "f32":
+        return np.asarray(a, dtype=np.float32).astype(np.float64)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+# ------------------------------------------------- distribution statistics --
+
+def distribution_stats(z: np.ndarray) -> dict:
+    """Softmax statistics of logit rows ``z[..., V]`` (temperature 1).
+
+    argmax: lowest index of the maximum logit; conf: largest probability;
+    entropy: Eq. (1), ``-sum p log p`` with ``0 log 0 = 0``, in nats."""
+    z = np.asarray(z, dtype=np.float64)
+    m = z.max(axis=-1, keepdims=True)
+    y = z.argmax(axis=-1)                      # first maximum = lowest index
+    e = np.exp(z - m)
+    p = e / e.sum(axis=-1, keepdims=True)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        plogp = np.where(p > 0.0, p * np.log(np.where(p > 0.0, p, 1.0)), 0.0)
+    plogp = np.where(np.isnan(p), np.nan, plogp)
+    return {
+        "argmax": y.astype(np.int64),
+        "conf": p.max(axis=-1),
+        "entropy": -plogp.sum(axis=-1),
+        "p": p,
+    }
+
+
+def _top2_gap(z: np.ndarray, y: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
+    """Gap between the top logit and the best other logit, and that runner-up."""
+    zz = z.copy()
+    np.put_along_axis(zz, y[..., None], -np.inf, axis=-1)
+    second = zz.argmax(axis=-1)
+    gap = np.take_along_axis(z, y[..., None], -1)[..., 0] - np.take_along_axis(z, second[..., None], -1)[..., 0]
+    return gap, second
+
+
+def project_layer_stats(hidden: np.ndarray, w_u: np.ndarray, dtype: str,
+                        positions: list[tuple[int, int]], w_rows_per_chunk: int = 8192,
+                        max_bytes: int = 1 << 30) -> dict:
+    """Per-layer statistics at the given canvas positions.
+
+    For each position (b, i) and each supplied layer l the logits are
+    ``z = W_U x`` with ``x = hidden[l][b][i]`` (Section 2.2: intermediate
+    states read out through the output head; Appendix A.6: only masked
+    positions are projected). Returns arrays shaped [npos][K]:
+    ``argmax, conf, entropy`` of each layer's distribution, ``p_final`` =
+    probability at layer l of the final layer's argmax token, and two
+    diagnostics for classifying near-ties: ``gap`` (top-1 minus top-2 logit)
+    and ``absbound`` (max over the top two tokens v of sum_k |W_U[v,k] x_k|)."""
+    K = hidden.shape[0]
+    V, d = w_u.shape
+    npos = len(positions)
+    out = {k: np.zeros((npos, K), np.float64) for k in ("conf", "entropy", "p_final", "gap", "absbound")}
+    out["argmax"] = np.zeros((npos, K), np.int64)
+    if npos == 0:
+        return out
+    per_block = max(1, int(max_bytes // (K * V * 8)))
+    for p0 in range(0, npos, per_block):
+        blk = positions[p0:p0 + per_block]
+        nb = len(blk)
+        x = np.stack([to_f64(hidden[l, b, i], dtype) for (b, i) in blk for l in range(K)])  # [nb*K][d]
+        z = np.empty((nb * K, V), np.float64)
+        for v0 in range(0, V, w_rows_per_chunk):
+            wc = to_f64(w_u[v0:v0 + w_rows_per_chunk], dtype)
+            z[:, v0:v0 + wc.shape[0]] = x @ wc.T
+        z = z.reshape(nb, K, V)
+        st = distribution_stats(z)
+        y_final = st["argmax"][:, K - 1]
+        gap, second = _top2_gap(z, st["argmax"])
+        absb = np.zeros((nb, K))
+        for a in range(nb):
+            for l in range(K):
+                xr = np.abs(x[a * K + l])
+                rows = to_f64(w_u[[st["argmax"][a, l], second[a, l]]], dtype)
+                absb[a, l] = (np.abs(rows) @ xr).max()
+        sl = slice(p0, p0 + nb)
+        out["argmax"][sl] = st["argmax"]
+        out["conf"][sl] = st["conf"]
+        out["entropy"][sl] = st["entropy"]
+        out["p_final"][sl] = np.take_along_axis(st["p"], y_final[:, None, None].repeat(K, 1), -1)[..., 0]
+        out["gap"][sl] = gap
+        out["absbound"][sl] = absb
+    return out
+
+
+# ------------------------------------------------------ layerwise stability --
+
+def persistence(layer_argmax: np.ndarray) -> int:
+    """Eq. (2): number of consecutive layers, ending at the final one, whose
+    argmax equals the final prediction; the count stops at the first
+    disagreement (earlier agreeing layers are not counted)."""
+    K = len(layer_argmax)
+    y = layer_argmax[K - 1]
+    k = 1
+    while k < K and layer_argmax[K - 1 - k] == y:
+        k += 1
+    return k
+
+
+def confidence_drop(p_final: np.ndarray, k_i: int) -> float:
+    """Eq. (3): peak over the agreement suffix of the final token's
+    probability, minus its final-layer probability."""
+    K = len(p_final)
+    return float(max(p_final[K - k_i:]) - p_final[K - 1])
+
+
+def stability_score(k_i: int, r_i: float, p: Params) -> float:
+    """Eq. (4)."""
+    return float(min(k_i, p.k_max)) - p.w * r_i
+
+
+def candidate_routes(c: float, s: float, p: Params) -> tuple[bool, bool]:
+    """Eq. (5): (high-confidence route, stability route). NaN fails both."""
+    high = bool(c >= p.theta_h)
+    stab = bool(p.theta_c <= c < p.theta_h and s >= p.theta_s)
+    return high, stab
+
+
+# ------------------------------------------------------------ commitment --
+
+def commit_scan(H: np.ndarray, cand: np.ndarray, c: np.ndarray, p: Params) -> dict:
+    """Section 3.2 for one sequence, on its masked positions in canvas order.
+
+    Literal left-to-right construction: when the scan reaches position i,
+    ``E_i`` is the entropy summed over earlier masked positions not yet
+    selected (non-candidates and rejected candidates alike); a candidate is
+    selected when ``E_i <= beta``. If nothing is selected, the single most
+    confident of the first W masked positions is committed (progress
+    fallback). Returns ``commit`` (bool), ``E`` (E_i at every masked
+    position, before the fallback) and ``fallback`` (index or -1)."""
+    n = len(H)
+    commit = np.zeros(n, bool)
+    E = np.zeros(n, np.float64)
+    acc = 0.0  # sum of H over earlier masked positions left out of A
+    for i in range(n):
+        E[i] = acc
+        if cand[i] and acc <= p.beta:
+            commit[i] = True
+        else:
+            acc = acc + H[i]
+    fb = -1
+    if n > 0 and not commit.any():
+        win = c[:min(p.window, n)]
+        best = -np.inf
+        fb = 0
+        for j, cj in enumerate(win):
+            if not np.isnan(cj) and cj > best:
+                best, fb = cj, j
+        commit[fb] = True
+    return {"commit": commit, "E": E, "fallback": fb}
+
+
+def commit_closed_form(H: np.ndarray, cand: np.ndarray, p: Params) -> dict:
+    """Equivalent closed form of the budget test: with
+    ``N_i = sum of H_j over earlier masked non-candidates``, the selected set
+    is exactly ``{i : cand_i and N_i <= beta}`` (every earlier candidate of an
+    accepted one is accepted, so ``E_i = N_i`` there; a rejected one has
+    ``E_i >= N_i > beta``). Returned without the fallback."""
+    n = len(H)
+    N = np.zeros(n, np.float64)
+    acc = 0.0
+    for i in range(n):
+        N[i] = acc
+        if not cand[i]:
+            acc = acc + H[i]
+    return {"commit": np.asarray(cand, bool) & (N <= p.beta), "N": N}
+
+
+# ------------------------------------------------------------- assembly --
+
+def select(mask: np.ndarray, layer: dict, p: Params, positions: list[tuple[int, int]]) -> dict:
+    """Scoring (Eq. 2-5) and commitment (Section 3.2) from per-layer
+    statistics ``layer[name][npos][K]`` listed in ``positions`` order, which
+    must hold every masked position of every sequence in canvas order."""
+    B, L = mask.shape
+    K = layer["argmax"].shape[1]
+    o = {
+        "commit": np.zeros((B, L), np.uint8),
+        "token": np.full((B, L), -1, np.int32),
+        "entropy": np.zeros((B, L)),
+        "confidence": np.zeros((B, L)),
+        "persistence": np.zeros((B, L), np.int32),
+        "drop": np.zeros((B, L)),
+        "stability": np.zeros((B, L)),
+        "flags": np.zeros((B, L), np.uint8),
+        "upstream_entropy": np.zeros((B, L)),
+        "budget_prefix": np.zeros((B, L)),
+        "n_commit": np.zeros(B, np.int32),
+    }
+    index = {bi: a for a, bi in enumerate(positions)}
+    for b in range(B):
+        masked = np.nonzero(mask[b])[0]
+        n = len(masked)
+        H = np.zeros(n)
+        c = np.zeros(n)
+        cand = np.zeros(n, bool)
+        for q, i in enumerate(masked):
+            a = index[(b, int(i))]
+            am = layer["argmax"][a]
+            pf = layer["p_final"][a]
+            k_i = persistence(am)
+            r_i = confidence_drop(pf, k_i)
+            s_i = stability_score(k_i, r_i, p)
+            c_i = layer["conf"][a, K - 1]
+            h_i = layer["entropy"][a, K - 1]
+            high, stab = candidate_routes(c_i, s_i, p)
+            H[q], c[q], cand[q] = h_i, c_i, high or stab
+            o["token"][b, i] = am[K - 1]
+            o["entropy"][b, i] = h_i
+            o["confidence"][b, i] = c_i
+            o["persistence"][b, i] = k_i
+            o["drop"][b, i] = r_i
+            o["stability"][b, i] = s_i
+            o["flags"][b, i] = (FLAG_CANDIDATE * (high or stab)) | (FLAG_HIGH_CONF * high) | (FLAG_STABLE * stab)
+        sc = commit_scan(H, cand, c, p)
+        cf = commit_closed_form(H, cand, p)
+        if not np.isnan(H).any():
+            pre = sc["commit"].copy()
+            if sc["fallback"] >= 0:
+                pre[sc["fallback"]] = False
+            assert np.array_equal(pre, cf["commit"]), "sequential scan and closed form disagree"
+        for q, i in enumerate(masked):
+            o["upstream_entropy"][b, i] = sc["E"][q]
+            o["budget_prefix"][b, i] = cf["N"][q]
+            if sc["commit"][q]:
+                o["commit"][b, i] = 1
+                o["flags"][b, i] |= FLAG_COMMITTED
+        if sc["fallback"] >= 0:
+            o["flags"][b, masked[sc["fallback"]]] |= FLAG_FALLBACK
+        o["n_commit"][b] = int(sc["commit"].sum())
+    return o
+
+
+def masked_positions(mask: np.ndarray) -> list[tuple[int, int]]:
+    B, L = mask.shape
+    return [(b, int(i)) for b in range(B) for i in np.nonzero(mask[b])[0]]
+
+
+def score_commit(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params) -> dict:
+    """The whole commit step for one decoding iteration: project every masked
+    position at every supplied layer, score, select candidates and commit.
+    ``hidden[K][B][L][d]``, ``w_u[V][d]``, ``mask[B][L]`` (1 = masked)."""
+    pos = masked_positions(mask)
+    layer = project_layer_stats(hidden, w_u, dtype, pos)
+    o = select(mask, layer, p, pos)
+    K = hidden.shape[0]
+    B, L = mask.shape
+    for name in ("argmax", "conf", "entropy", "p_final", "gap", "absbound"):
+        arr = np.full((K, B, L), -1 if name == "argmax" else 0.0,
+                      np.int64 if name == "argmax" else np.float64)
+        for a, (b, i) in enumerate(pos):
+            arr[:, b, i] = layer[name][a]
+        o["layer_" + name] = arr
+    return o
