@@ -1,0 +1,216 @@
+"""Benchmark of the RPD commit step on one MI355X.
+
+One step = one call of the whole commit step (masked-position compaction,
+logit-lens projection with fused softmax statistics, cross-tile reduction
+and stability scoring, budgeted commitment) on a seeded synthetic batch that
+is resident in HBM before timing starts. Prints ONE JSON line on stdout;
+progress goes to stderr.
+
+Default workload: late decoding at the LLaDA-8B shape (d=4096, V=126464,
+bf16, one 256-position canvas with 8 masked positions, the final K=4
+layers), the regime where streaming the 1.04 GB unembedding bounds the step.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
+RIDGE_ROWS = 315             # projected rows where the projection turns compute-bound
+
+METRIC = "masked positions scored+committed/sec at LLaDA-8B shape; MFMA % / HBM GB/s"
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_36452_amd", "csrc", "rpd_kernels.hip")
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_sha() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def read_traffic(workload: str):
+    """HBM bytes per projection launch from the committed rocprofv3 counter
+    summary of this workload, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"k_proj_bf16_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha") != kernel_source_sha():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
+        if n:
+            return int(max(n))
+    except Exception:
+        pass
+    return os.cpu_count() or 1
+
+
+def cpu_baseline(w, P, budget_s: float) -> dict:
+    """The fp64 oracle, as it is, on the host cores over a bounded sample of
+    the same workload: whole calls of the step while they fit the budget,
+    else a prefix of its masked positions."""
+    import numpy as np
+    import oracle as O
+    pos_all = O.masked_positions(w.mask)
+    t0 = time.perf_counter()
+    pos, layer = O.layer_stats_masked(w.hidden, w.w_u, w.mask, w.cfg.dtype)
+    O.assemble(w.mask, pos, layer, P)
+    t = time.perf_counter() - t0
+    reps = 1
+    while t * (reps + 1) / reps < budget_s and reps < 8:
+        t0 = time.perf_counter()
+        pos, layer = O.layer_stats_masked(w.hidden, w.w_u, w.mask, w.cfg.dtype)
+        O.assemble(w.mask, pos, layer, P)
+        t += time.perf_counter() - t0
+        reps += 1
+    n = len(pos_all)
+    return {"value": n * reps / t, "unit": "positions/s", "cores": blas_threads(), "kind": "oracle",
+            "sample": f"{reps} whole call(s) of the step ({n} masked positions x {w.cfg.K} layers, "
+                      f"V={w.cfg.V}, d={w.cfg.d}) in float64, {t:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="llada_late")
+    ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--rule", default="strict", choices=["strict", "llada", "dream"])
+    ap.add_argument("--beta", type=float, default=1.0)
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the commit step is benchmarked on a single MI355X "
+              f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    from paper_2609_36452_amd import binding as rpd
+    from paper_2609_36452_amd.workload import CONFIGS, make_workload
+
+    if not os.path.exists(rpd._LIB_PATH):
+        from paper_2609_36452_amd.build import build
+        build()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = CONFIGS[args.config]
+    log(f"drawing workload {cfg.name} seed {args.seed}")
+    t0 = time.perf_counter()
+    w = make_workload(cfg, args.seed)
+    log(f"  drawn in {time.perf_counter() - t0:.1f} s; masked positions {w.n_masked}")
+    if args.rule == "strict":
+        P = rpd.Params.strict(cfg.K, args.beta)
+    elif args.rule == "llada":
+        P = rpd.Params.llada()
+    else:
+        P = rpd.Params.dream()
+    dev = torch.device("cuda:0")
+    if cfg.dtype == "bf16":
+        hidden = torch.from_numpy(w.hidden).view(torch.bfloat16).to(dev)
+        w_u = torch.from_numpy(w.w_u).view(torch.bfloat16).to(dev)
+    else:
+        hidden = torch.from_numpy(w.hidden).to(dev)
+        w_u = torch.from_numpy(w.w_u).to(dev)
+    mask = torch.from_numpy(w.mask).to(dev)
+    call = rpd.ScoreCommit(hidden, w_u, mask, P, max_masked=w.n_masked)
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup}")
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    proj_a = [ev() for _ in range(K)]
+    proj_b = [ev() for _ in range(K)]
+    start, end = ev(), ev()
+    log(f"timing {K} steps")
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    start.record()
+    for k in range(K):
+        call(events=[None, proj_a[k], proj_b[k]])
+    end.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall0
+    ms_total = start.elapsed_time(end)
+    ms_step = ms_total / K
+    proj_ms = [a.elapsed_time(b) for a, b in zip(proj_a, proj_b)]
+    proj_avg = float(np.mean(proj_ms))
+    n = w.n_masked
+    R = n * cfg.K
+    value = n * K / (ms_total / 1e3)
+    log(f"  {ms_step * 1e3:.1f} us/step, projection {proj_avg * 1e3:.1f} us (median "
+        f"{np.median(proj_ms) * 1e3:.1f}), wall {t_wall:.3f} s")
+
+    bytes_alg = cfg.V * cfg.d * (2 if cfg.dtype == "bf16" else 4) + R * cfg.d * (2 if cfg.dtype == "bf16" else 4)
+    flops_alg = 2.0 * R * cfg.V * cfg.d
+    if R < RIDGE_ROWS:
+        achieved = bytes_alg / (proj_avg / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    else:
+        achieved = flops_alg / (proj_avg / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4)}
+    roof["traffic"] = read_traffic(cfg.name)
+    roof["kernel"] = "k_proj_bf16" if cfg.dtype == "bf16" else "k_proj_f32"
+    roof["kernel_us"] = round(proj_avg * 1e3, 2)
+    roof["alg_bytes_per_launch"] = bytes_alg
+    roof["alg_flops_per_launch"] = flops_alg
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded random W_U ~ N(0,1/d) and hidden states of the model shape)",
+        "config": {"workload": f"{cfg.name}: d={cfg.d} V={cfg.V} B={cfg.B} L={cfg.L} K={cfg.K} "
+                               f"masked={n} ({R} projected rows), rule={args.rule} beta={P.beta}",
+                   "masked_positions": n, "projected_rows": R, "seed": args.seed},
+        "iterations_per_s": round(1e3 / ms_step, 1),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        import oracle as O
+        OP = O.Params(**P.__dict__)
+        log("cpu baseline (oracle)")
+        out["cpu_baseline"] = cpu_baseline(w, OP, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,208 @@
+/*
+ * rpd.h -- C ABI of the MI355X (gfx950) commit step of Reliable Parallel
+ * Decoding (RPD).
+ *
+ * One call performs one decoding iteration's commit step (Sections 2.2, 3.1
+ * and 3.2 of the paper; Appendix A.6 "Layerwise projection"): every masked
+ * canvas position is projected through the unembedding at each of the final
+ * K layers, each layer's full-vocabulary softmax is reduced to its argmax,
+ * top probability and entropy (Eq. 1), layerwise stability is scored
+ * (persistence Eq. 2, confidence drop Eq. 3, stability Eq. 4), candidates
+ * are formed (Eq. 5), and the candidates whose cumulative upstream entropy
+ * stays within the budget are committed, with the progress fallback
+ * (Section 3.2).
+ *
+ * Conventions for every entry point:
+ *  - Pointers marked "device" are HIP device (or managed) memory on the
+ *    current device; "host" pointers are read during the call only.
+ *  - The caller owns every buffer. The library allocates no device memory,
+ *    keeps no pointer after it returns, and never writes its inputs.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL = the
+ *    default stream). Results are valid once the stream has completed.
+ *  - Arrays are dense and row-major in the shapes given. The final layer of
+ *    the window is layer K-1.
+ *  - Errors: every argument is validated on the host before anything is
+ *    enqueued; on a non-OK status nothing was enqueued and the outputs are
+ *    untouched. rpd_last_error() then describes the failure (thread-local).
+ *    No C++ exception crosses this interface.
+ *  - Calls on distinct streams with distinct workspaces may overlap.
+ */
+#ifndef RPD_H
+#define RPD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RPD_ABI_VERSION 1
+
+/* element type of `hidden` and `w_u` (both must have the same type) */
+enum { RPD_DTYPE_BF16 = 0, RPD_DTYPE_F32 = 1 };
+
+typedef enum rpd_status {
+  RPD_OK = 0,
+  RPD_ERR_NULL_POINTER = 1,        /* a required pointer is NULL */
+  RPD_ERR_BAD_SHAPE = 2,           /* a dimension is out of range */
+  RPD_ERR_BAD_PARAM = 3,           /* a hyperparameter is out of range or NaN */
+  RPD_ERR_WORKSPACE_TOO_SMALL = 4, /* workspace_bytes < the required size */
+  RPD_ERR_UNSUPPORTED = 5,         /* dtype / alignment / size not supported */
+  RPD_ERR_HIP = 6                  /* a HIP runtime call or launch failed */
+} rpd_status;
+
+/* per-position flag bits written to rpd_outputs.flags */
+#define RPD_FLAG_CANDIDATE 1u  /* in the candidate set C_t (Eq. 5) */
+#define RPD_FLAG_HIGH_CONF 2u  /* admitted because c_i >= theta_h */
+#define RPD_FLAG_STABLE    4u  /* admitted through the stability test */
+#define RPD_FLAG_COMMITTED 8u  /* in the commitment set A_t */
+#define RPD_FLAG_FALLBACK  16u /* committed by the progress fallback */
+
+/* bits of the optional device status word */
+#define RPD_DEVICE_STATUS_MASKED_OVERFLOW 1 /* more masked positions than max_masked */
+
+/*
+ * The problem of one call (Section 3: the masked positions M_t of the canvas
+ * and the hidden states of the final layers of one forward pass).
+ *   K           number of final layers supplied, 1 <= K <= 64 (the paper
+ *               projects layers l0..L, Appendix A.6; here the K supplied)
+ *   B, L        sequences and canvas positions per sequence (B >= 1, L >= 1,
+ *               B*L <= 2^24)
+ *   d, V        hidden size and vocabulary size (1 <= d, 1 <= V < 2^31);
+ *               bf16 requires d % 8 == 0
+ *   dtype       RPD_DTYPE_BF16 or RPD_DTYPE_F32
+ *   hidden      device [K][B][L][d]; hidden states already passed through the
+ *               model's final normalisation; rows of unmasked positions are
+ *               never read (they may hold anything, NaN included)
+ *   w_u         device [V][d]; the unembedding (output head), d contiguous;
+ *               16-byte aligned
+ *   mask        device [B][L] uint8; nonzero = masked (in M_t)
+ *   max_masked  an upper bound on the number of masked positions summed over
+ *               the batch, or -1. With -1 the call reads the exact count back
+ *               from the device once (one stream synchronisation). If the
+ *               bound is exceeded, only the first max_masked masked positions
+ *               (batch-major, canvas order) are scored, the results for the
+ *               rest are undefined, and RPD_DEVICE_STATUS_MASKED_OVERFLOW is
+ *               raised in the optional status word.
+ */
+typedef struct rpd_problem {
+  int32_t K, B, L, d, V;
+  int32_t dtype;
+  const void* hidden;
+  const void* w_u;
+  const uint8_t* mask;
+  int32_t max_masked;
+} rpd_problem;
+
+/*
+ * Hyperparameters (Table 4, Appendix A.6; LLaDA: theta_s 3.5, w 15; Dream:
+ * theta_s 2.5, w 20; both theta_h 0.9, theta_c 0.6, K_max 6, beta 4 nats,
+ * W 32). Requirements: 0 <= theta_c <= theta_h, w >= 0, k_max >= 1,
+ * beta >= 0 (may be +inf), window >= 1, flags == 0 (reserved); no NaN.
+ */
+typedef struct rpd_params {
+  float theta_h;   /* high-confidence threshold (bypasses stability), Eq. 5 */
+  float theta_c;   /* minimum confidence for stability admission, Eq. 5 */
+  float theta_s;   /* stability threshold, Eq. 5 */
+  float w;         /* weight of the confidence-drop penalty, Eq. 4 */
+  int32_t k_max;   /* cap on persistence, Eq. 4 */
+  float beta;      /* cumulative entropy budget in nats, Section 3.2 */
+  int32_t window;  /* fallback window W, Section 3.2 */
+  uint32_t flags;  /* reserved, must be 0 */
+} rpd_params;
+
+/*
+ * Outputs, all device memory, shape [B][L] unless noted. Unmasked positions
+ * receive: commit 0, token -1, persistence 0, flags 0 and 0.0f elsewhere.
+ *   commit            1 if the position is in A_t (Section 3.2)
+ *   token             y_i, the final-layer argmax (lowest index on ties),
+ *                     for every masked position, committed or not
+ *   entropy           H(p_i^(K-1)) in nats (Eq. 1)
+ *   confidence        c_i = p_i^(K-1)(y_i)
+ *   persistence       K_i (Eq. 2), counted within the K supplied layers
+ *   drop              r_i (Eq. 3)
+ *   stability         S_i = min(K_i, k_max) - w r_i (Eq. 4)
+ *   flags             RPD_FLAG_* bits
+ *   upstream_entropy  E_i: entropy summed over earlier masked positions of
+ *                     the sequence that are not in A_t (Section 3.2),
+ *                     evaluated before the fallback
+ *   n_commit          [B] number of committed positions per sequence
+ * Optional (NULL to skip):
+ *   layer_argmax, layer_conf, layer_entropy   [K][B][L] per-layer argmax,
+ *                     top probability and entropy at masked positions
+ *                     (unmasked entries are left untouched)
+ *   status            one int32 of RPD_DEVICE_STATUS_* bits, overwritten
+ */
+typedef struct rpd_outputs {
+  uint8_t* commit;
+  int32_t* token;
+  float* entropy;
+  float* confidence;
+  int32_t* persistence;
+  float* drop;
+  float* stability;
+  uint8_t* flags;
+  float* upstream_entropy;
+  int32_t* n_commit;
+  int32_t* layer_argmax;
+  float* layer_conf;
+  float* layer_entropy;
+  int32_t* status;
+} rpd_outputs;
+
+/* Device workspace bytes that rpd_score_commit needs for problem `p`
+ * (pointers in `p` are not read). Returns 0 if the shape is invalid. */
+size_t rpd_workspace_size(const rpd_problem* p);
+
+/*
+ * The whole commit step (Sections 2.2, 3.1, 3.2). `workspace` is device
+ * memory of at least rpd_workspace_size(p) bytes, 256-byte aligned, used only
+ * during the call's stream work; its prior contents do not matter.
+ */
+rpd_status rpd_score_commit(const rpd_problem* p, const rpd_params* q, const rpd_outputs* o,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * rpd_score_commit, recording caller-created HIP events (hipEvent_t, cast to
+ * void*) on `stream` at its stage boundaries, for callers that time the
+ * stages: events[0] before the masked-position compaction, [1] before the
+ * projection (logit lens + fused softmax statistics), [2] after it, [3]
+ * after the cross-tile reduction and stability scoring, [4] after the
+ * commitment scan. Only the first n_events (0..5) are used; NULL entries
+ * are skipped. Everything else is exactly rpd_score_commit.
+ */
+rpd_status rpd_score_commit_timed(const rpd_problem* p, const rpd_params* q, const rpd_outputs* o,
+                                  void* workspace, size_t workspace_bytes, void* stream,
+                                  void* const* events, int32_t n_events);
+
+/*
+ * Scoring and commitment from per-layer statistics that the caller already
+ * has (Eq. 2-5 and Section 3.2), for callers whose logits come from
+ * elsewhere. layer_argmax / layer_conf / layer_entropy are device [K][B][L]
+ * in the layout rpd_score_commit writes them (only masked positions are
+ * read; only the final layer's entropy is used). Inside the agreement suffix
+ * the probability of the final token equals that layer's top probability,
+ * which is how Eq. 3 is evaluated. Writes the required outputs of `o`; the
+ * optional per-layer pointers and status of `o` are ignored. Needs no
+ * workspace.
+ */
+rpd_status rpd_gate_commit(int32_t K, int32_t B, int32_t L, const uint8_t* mask,
+                           const int32_t* layer_argmax, const float* layer_conf,
+                           const float* layer_entropy, const rpd_params* q,
+                           const rpd_outputs* o, void* stream);
+
+/* Static text for a status code. */
+const char* rpd_status_string(rpd_status s);
+
+/* Detail of the calling thread's most recent non-OK status ("" if none). */
+const char* rpd_last_error(void);
+
+/* RPD_ABI_VERSION of the library. */
+int32_t rpd_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RPD_H */

@@ -314,14 +314,16 @@ def masked_positions(mask: np.ndarray) -> list[tuple[int, int]]:
     return [(b, int(i)) for b in range(B) for i in np.nonzero(mask[b])[0]]
 
 
-def score_commit(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params) -> dict:
-    """The whole commit step for one decoding iteration: project every masked
-    position at every supplied layer, score, select candidates and commit.
-    ``hidden[K][B][L][d]``, ``w_u[V][d]``, ``mask[B][L]`` (1 = masked)."""
+def layer_stats_masked(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str):
+    """Per-layer statistics of every masked position (canvas order)."""
     pos = masked_positions(mask)
-    layer = project_layer_stats(hidden, w_u, dtype, pos)
+    return pos, project_layer_stats(hidden, w_u, dtype, pos)
+
+
+def assemble(mask: np.ndarray, pos: list, layer: dict, p: Params) -> dict:
+    """Scoring and commitment plus the per-layer arrays in [K][B][L] layout."""
     o = select(mask, layer, p, pos)
-    K = hidden.shape[0]
+    K = layer["argmax"].shape[1]
     B, L = mask.shape
     for name in ("argmax", "conf", "entropy", "p_final", "gap", "absbound"):
         arr = np.full((K, B, L), -1 if name == "argmax" else 0.0,
@@ -330,3 +332,11 @@ def score_commit(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: s
             arr[:, b, i] = layer[name][a]
         o["layer_" + name] = arr
     return o
+
+
+def score_commit(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params) -> dict:
+    """The whole commit step for one decoding iteration: project every masked
+    position at every supplied layer, score, select candidates and commit.
+    ``hidden[K][B][L][d]``, ``w_u[V][d]``, ``mask[B][L]`` (1 = masked)."""
+    pos, layer = layer_stats_masked(hidden, w_u, mask, dtype)
+    return assemble(mask, pos, layer, p)

@@ -1,0 +1,245 @@
+// C ABI of the RPD commit step: argument validation, workspace layout,
+// launch planning and error reporting. Kernels live in rpd_kernels.hip.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "rpd.h"
+#include "rpd_launch.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+rpd_status fail(rpd_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+constexpr size_t kHeaderBytes = 256;   // n_masked, device status
+constexpr long long kMaxBL = 1LL << 24;
+constexpr int kMaxK = 64;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool shape_ok(const rpd_problem* p) {
+  return p->K >= 1 && p->K <= kMaxK && p->B >= 1 && p->L >= 1 && (long long)p->B * p->L <= kMaxBL && p->d >= 1 &&
+         p->V >= 1 && p->V < 0x7fffffff;
+}
+
+long long masked_cap(const rpd_problem* p) {
+  const long long BL = (long long)p->B * p->L;
+  return (p->max_masked < 0 || p->max_masked > BL) ? BL : p->max_masked;
+}
+
+size_t partial_bytes(const rpd::ProjPlan& pl, long long rows) { return (size_t)rows * pl.nvt * 16; }
+
+// Bytes for the plan chosen at `cap` masked positions; when the exact count
+// is read back later (max_masked < 0) any smaller count may be planned, so
+// the small-row variants are covered too.
+size_t workspace_bytes_for(const rpd_problem* p, long long cap) {
+  const long long rows = (long long)p->K * cap;
+  size_t part = partial_bytes(rpd::plan_projection(p->dtype, rows, p->V), rows);
+  if (p->max_masked < 0) {
+    for (long long r : {32LL, 64LL, 65LL}) {
+      const long long rr = r < rows ? r : rows;
+      const size_t b = partial_bytes(rpd::plan_projection(p->dtype, rr, p->V), rr);
+      if (b > part) part = b;
+    }
+  }
+  return kHeaderBytes + align256((size_t)((long long)p->B * p->L) * 4) + align256(part);
+}
+
+rpd_status check_params(const rpd_params* q) {
+  if (!q) return fail(RPD_ERR_NULL_POINTER, "params is NULL");
+  const float f[] = {q->theta_h, q->theta_c, q->theta_s, q->w};
+  for (float v : f)
+    if (!std::isfinite(v)) return fail(RPD_ERR_BAD_PARAM, "theta_h, theta_c, theta_s and w must be finite");
+  if (!(q->theta_c >= 0.f && q->theta_c <= q->theta_h))
+    return fail(RPD_ERR_BAD_PARAM, "need 0 <= theta_c <= theta_h (got %g, %g)", q->theta_c, q->theta_h);
+  if (q->w < 0.f) return fail(RPD_ERR_BAD_PARAM, "w must be >= 0 (got %g)", q->w);
+  if (q->k_max < 1) return fail(RPD_ERR_BAD_PARAM, "k_max must be >= 1 (got %d)", q->k_max);
+  if (std::isnan(q->beta) || q->beta < 0.f) return fail(RPD_ERR_BAD_PARAM, "beta must be >= 0 (got %g)", q->beta);
+  if (q->window < 1) return fail(RPD_ERR_BAD_PARAM, "window must be >= 1 (got %d)", q->window);
+  if (q->flags != 0) return fail(RPD_ERR_BAD_PARAM, "flags is reserved and must be 0");
+  return RPD_OK;
+}
+
+rpd_status check_outputs(const rpd_outputs* o) {
+  if (!o) return fail(RPD_ERR_NULL_POINTER, "outputs is NULL");
+  if (!o->commit || !o->token || !o->entropy || !o->confidence || !o->persistence || !o->drop || !o->stability ||
+      !o->flags || !o->upstream_entropy || !o->n_commit)
+    return fail(RPD_ERR_NULL_POINTER, "a required output pointer is NULL");
+  const int nl = (o->layer_argmax != nullptr) + (o->layer_conf != nullptr) + (o->layer_entropy != nullptr);
+  if (nl != 0 && nl != 3)
+    return fail(RPD_ERR_NULL_POINTER, "layer_argmax, layer_conf and layer_entropy must be all set or all NULL");
+  return RPD_OK;
+}
+
+void fill_common(rpd::Launch& a, const rpd_params* q, const rpd_outputs* o) {
+  a.theta_h = q->theta_h;
+  a.theta_c = q->theta_c;
+  a.theta_s = q->theta_s;
+  a.w = q->w;
+  a.beta = q->beta;
+  a.k_max = q->k_max;
+  a.window = q->window;
+  a.commit = o->commit;
+  a.token = o->token;
+  a.entropy = o->entropy;
+  a.confidence = o->confidence;
+  a.persistence = o->persistence;
+  a.drop = o->drop;
+  a.stability = o->stability;
+  a.flags = o->flags;
+  a.upstream_entropy = o->upstream_entropy;
+  a.n_commit = o->n_commit;
+  a.layer_argmax = o->layer_argmax;
+  a.layer_conf = o->layer_conf;
+  a.layer_entropy = o->layer_entropy;
+  a.user_status = o->status;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t rpd_workspace_size(const rpd_problem* p) {
+  if (!p || !shape_ok(p) || (p->dtype != RPD_DTYPE_BF16 && p->dtype != RPD_DTYPE_F32)) return 0;
+  return workspace_bytes_for(p, masked_cap(p));
+}
+
+static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, const rpd_outputs* o,
+                                    void* workspace, size_t workspace_bytes, void* stream, void* const* events,
+                                    int32_t n_events) {
+  g_err[0] = '\0';
+  if (!p) return fail(RPD_ERR_NULL_POINTER, "problem is NULL");
+  if (!p->hidden || !p->w_u || !p->mask) return fail(RPD_ERR_NULL_POINTER, "hidden, w_u and mask are required");
+  if (!shape_ok(p))
+    return fail(RPD_ERR_BAD_SHAPE, "need 1<=K<=%d, B,L>=1, B*L<=2^24, d>=1, 1<=V<2^31-1 (got K=%d B=%d L=%d d=%d V=%d)",
+                kMaxK, p->K, p->B, p->L, p->d, p->V);
+  if (p->dtype != RPD_DTYPE_BF16 && p->dtype != RPD_DTYPE_F32)
+    return fail(RPD_ERR_UNSUPPORTED, "dtype %d is not supported", p->dtype);
+  if (p->dtype == RPD_DTYPE_BF16) {
+    if (p->d % 8 != 0) return fail(RPD_ERR_UNSUPPORTED, "bf16 needs d %% 8 == 0 (got d=%d)", p->d);
+    if (((uintptr_t)p->hidden | (uintptr_t)p->w_u) & 15)
+      return fail(RPD_ERR_UNSUPPORTED, "bf16 hidden and w_u must be 16-byte aligned");
+  } else if (((uintptr_t)p->hidden | (uintptr_t)p->w_u) & 3) {
+    return fail(RPD_ERR_UNSUPPORTED, "fp32 hidden and w_u must be 4-byte aligned");
+  }
+  rpd_status st = check_params(q);
+  if (st != RPD_OK) return st;
+  st = check_outputs(o);
+  if (st != RPD_OK) return st;
+  if (n_events < 0 || n_events > 5 || (n_events > 0 && !events))
+    return fail(RPD_ERR_BAD_PARAM, "need 0 <= n_events <= 5 and a non-NULL events array");
+
+  const long long cap = masked_cap(p);
+  const size_t need = workspace_bytes_for(p, cap);
+  if (!workspace) return fail(RPD_ERR_NULL_POINTER, "workspace is NULL (%zu bytes needed)", need);
+  if ((uintptr_t)workspace & 255) return fail(RPD_ERR_UNSUPPORTED, "workspace must be 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(RPD_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  rpd::Launch a{};
+  a.K = p->K;
+  a.B = p->B;
+  a.L = p->L;
+  a.d = p->d;
+  a.V = p->V;
+  a.hidden = p->hidden;
+  a.w_u = p->w_u;
+  a.mask = p->mask;
+  a.max_masked = (int)cap;
+  a.n_masked = reinterpret_cast<int32_t*>(ws);
+  a.dev_status = reinterpret_cast<int32_t*>(ws + 4);
+  a.rows = reinterpret_cast<int32_t*>(ws + kHeaderBytes);
+  a.partials = reinterpret_cast<float4*>(ws + kHeaderBytes + align256((size_t)((long long)p->B * p->L) * 4));
+  fill_common(a, q, o);
+
+  auto mark = [&](int k) -> hipError_t {
+    if (k < n_events && events[k]) return hipEventRecord(static_cast<hipEvent_t>(events[k]), s);
+    return hipSuccess;
+  };
+  hipError_t e = mark(0);
+  if (e == hipSuccess) e = rpd::launch_compact(a, s);
+  if (e != hipSuccess) return fail(RPD_ERR_HIP, "compaction: %s", hipGetErrorString(e));
+  if (p->max_masked < 0) {
+    int32_t n = 0;
+    e = hipMemcpyAsync(&n, a.n_masked, sizeof n, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return fail(RPD_ERR_HIP, "reading the masked count: %s", hipGetErrorString(e));
+    a.max_masked = n;
+  }
+  a.plan = rpd::plan_projection(p->dtype, (long long)p->K * a.max_masked, p->V);
+  if ((e = mark(1)) == hipSuccess && (e = rpd::launch_projection(a, s)) == hipSuccess && (e = mark(2)) == hipSuccess &&
+      (e = rpd::launch_reduce_score(a, s)) == hipSuccess && (e = mark(3)) == hipSuccess &&
+      (e = rpd::launch_commit(a, s)) == hipSuccess)
+    e = mark(4);
+  if (e != hipSuccess) return fail(RPD_ERR_HIP, "launch: %s", hipGetErrorString(e));
+  return RPD_OK;
+}
+
+rpd_status rpd_score_commit(const rpd_problem* p, const rpd_params* q, const rpd_outputs* o, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  return score_commit_impl(p, q, o, workspace, workspace_bytes, stream, nullptr, 0);
+}
+
+rpd_status rpd_score_commit_timed(const rpd_problem* p, const rpd_params* q, const rpd_outputs* o,
+                                  void* workspace, size_t workspace_bytes, void* stream, void* const* events,
+                                  int32_t n_events) {
+  return score_commit_impl(p, q, o, workspace, workspace_bytes, stream, events, n_events);
+}
+
+rpd_status rpd_gate_commit(int32_t K, int32_t B, int32_t L, const uint8_t* mask, const int32_t* layer_argmax,
+                           const float* layer_conf, const float* layer_entropy, const rpd_params* q,
+                           const rpd_outputs* o, void* stream) {
+  g_err[0] = '\0';
+  if (!mask || !layer_argmax || !layer_conf || !layer_entropy)
+    return fail(RPD_ERR_NULL_POINTER, "mask and the three per-layer inputs are required");
+  if (K < 1 || K > kMaxK || B < 1 || L < 1 || (long long)B * L > kMaxBL)
+    return fail(RPD_ERR_BAD_SHAPE, "need 1<=K<=%d, B,L>=1, B*L<=2^24 (got K=%d B=%d L=%d)", kMaxK, K, B, L);
+  rpd_status st = check_params(q);
+  if (st != RPD_OK) return st;
+  st = check_outputs(o);
+  if (st != RPD_OK) return st;
+  rpd::Launch a{};
+  a.K = K;
+  a.B = B;
+  a.L = L;
+  a.mask = mask;
+  fill_common(a, q, o);
+  a.layer_argmax = nullptr;
+  a.layer_conf = nullptr;
+  a.layer_entropy = nullptr;
+  a.user_status = nullptr;
+  hipError_t e =
+      rpd::launch_gate_commit(a, layer_argmax, layer_conf, layer_entropy, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(RPD_ERR_HIP, "launch: %s", hipGetErrorString(e));
+  return RPD_OK;
+}
+
+const char* rpd_status_string(rpd_status s) {
+  switch (s) {
+    case RPD_OK: return "ok";
+    case RPD_ERR_NULL_POINTER: return "null pointer";
+    case RPD_ERR_BAD_SHAPE: return "bad shape";
+    case RPD_ERR_BAD_PARAM: return "bad parameter";
+    case RPD_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case RPD_ERR_UNSUPPORTED: return "unsupported";
+    case RPD_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* rpd_last_error(void) { return g_err; }
+
+int32_t rpd_abi_version(void) { return RPD_ABI_VERSION; }
+
+}  // extern "C"

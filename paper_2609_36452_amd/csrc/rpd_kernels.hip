@@ -1,0 +1,835 @@
+// gfx950 (CDNA4) kernels of the RPD commit step.
+//
+// Pipeline of one call (all on the caller's stream):
+//   k_compact       masked positions of the canvas -> compacted list
+//                   (only masked positions are projected, Appendix A.6)
+//   k_proj_bf16     logit-lens projection z = W_U x for every (masked
+//                   position, layer) row on the bf16 matrix cores, with the
+//                   softmax statistics folded in per vocabulary tile, so the
+//                   V-wide logits never reach memory (Section 2.2 readout;
+//                   Eq. 1 entropy)
+//   k_proj_f32      the same on the vector ALU for fp32 inputs
+//   k_reduce_score  merge of the per-tile statistics -> argmax, top
+//                   probability and entropy per layer; persistence (Eq. 2),
+//                   drop (Eq. 3), stability (Eq. 4) and candidacy (Eq. 5)
+//   k_commit        per sequence: budgeted cumulative-entropy commitment and
+//                   progress fallback (Section 3.2) as prefix scans
+//
+// The softmax statistics of a set of logits {z_v} are kept as
+//   m = max z, idx = lowest v with z_v = m, S = sum e^{z-m}, T = sum e^{z-m}(z-m)
+// from which top probability = 1/S and entropy = ln S - T/S. Two such states
+// over disjoint vocabulary ranges merge exactly (up to rounding) by rescaling
+// to the larger maximum; merges happen in a fixed order, so results are
+// bitwise reproducible run to run.
+#include <climits>
+#include <cmath>
+
+#include "rpd_launch.h"
+
+namespace rpd {
+namespace {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+constexpr unsigned kFlagCandidate = 1u, kFlagHigh = 2u, kFlagStable = 4u, kFlagCommitted = 8u,
+                   kFlagFallback = 16u;
+
+// ------------------------------------------------------------ soft state --
+
+struct Soft {
+  float m;
+  int idx;
+  float S;
+  float T;
+};
+
+__device__ __forceinline__ Soft soft_empty() {
+  Soft s;
+  s.m = -INFINITY;
+  s.idx = INT_MAX;
+  s.S = 0.f;
+  s.T = 0.f;
+  return s;
+}
+
+// S == 0 only for a state that has seen no vocabulary entry (a state with
+// one or more entries has S >= 1, or NaN).
+__device__ __forceinline__ Soft soft_merge(const Soft a, const Soft b) {
+  if (b.S == 0.f) return a;
+  if (a.S == 0.f) return b;
+  const float M = fmaxf(a.m, b.m);
+  const float da = a.m - M, db = b.m - M;
+  const float ea = __expf(da), eb = __expf(db);
+  Soft r;
+  r.m = M;
+  r.S = a.S * ea + b.S * eb;
+  r.T = (a.T + da * a.S) * ea + (b.T + db * b.S) * eb;
+  r.idx = (a.m > b.m) ? a.idx : ((b.m > a.m) ? b.idx : min(a.idx, b.idx));
+  return r;
+}
+
+__device__ __forceinline__ Soft soft_shfl_xor(const Soft s, int mask) {
+  Soft o;
+  o.m = __shfl_xor(s.m, mask);
+  o.idx = __shfl_xor(s.idx, mask);
+  o.S = __shfl_xor(s.S, mask);
+  o.T = __shfl_xor(s.T, mask);
+  return o;
+}
+
+__device__ __forceinline__ float4 soft_pack(const Soft s) {
+  return make_float4(s.m, __int_as_float(s.idx), s.S, s.T);
+}
+
+__device__ __forceinline__ Soft soft_unpack(const float4 v) {
+  Soft s;
+  s.m = v.x;
+  s.idx = __float_as_int(v.y);
+  s.S = v.z;
+  s.T = v.w;
+  return s;
+}
+
+// Statistics of N logits held by one lane, vocabulary indices increasing;
+// entries with valid == false are skipped. NaN logits never win the max and
+// turn S and T into NaN.
+template <int N>
+__device__ __forceinline__ Soft soft_from_values(const float (&z)[N], const int (&v)[N], const bool (&ok)[N]) {
+  Soft s = soft_empty();
+#pragma unroll
+  for (int e = 0; e < N; ++e)
+    if (ok[e] && z[e] > s.m) {
+      s.m = z[e];
+      s.idx = v[e];
+    }
+  float S = 0.f, T = 0.f;
+#pragma unroll
+  for (int e = 0; e < N; ++e)
+    if (ok[e]) {
+      const float dz = z[e] - s.m;
+      const float ex = __expf(dz);
+      S += ex;
+      T = fmaf(ex, dz, T);
+    }
+  s.S = S;
+  s.T = T;
+  return s;
+}
+
+// ------------------------------------------------------------ K0 compact --
+
+__global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ mask, int BL, int cap,
+                                                   int32_t* __restrict__ rows, int32_t* __restrict__ n_out,
+                                                   int32_t* __restrict__ dev_status,
+                                                   int32_t* __restrict__ user_status) {
+  __shared__ int wsum[16];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int carry = 0;
+  for (int base = 0; base < BL; base += blockDim.x) {
+    const int i = base + threadIdx.x;
+    const int f = (i < BL && mask[i] != 0) ? 1 : 0;
+    const unsigned long long bal = __ballot(f);
+    const int before = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[wid] = __popcll(bal);
+    __syncthreads();
+    int off = 0, tot = 0;
+    for (int w = 0; w < nw; ++w) {
+      const int c = wsum[w];
+      off += (w < wid) ? c : 0;
+      tot += c;
+    }
+    const int pos = carry + off + before;
+    if (f && pos < cap) rows[pos] = i;
+    carry += tot;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    int st = 0, n = carry;
+    if (n > cap) {
+      st |= 1;
+      n = cap;
+    }
+    *n_out = n;
+    *dev_status = st;
+    if (user_status) *user_status = st;
+  }
+}
+
+// ----------------------------------------------------- K1 projection bf16 --
+
+// Map a workgroup to (row tile, vocab tile). Consecutive workgroup ids are
+// dispatched round-robin over the 8 XCDs, so id % 8 selects the XCD and the
+// jobs of one XCD are laid out so that its concurrently running workgroups
+// share operands in that XCD's L2: with many row tiles each XCD owns a block
+// of row tiles and sweeps the vocabulary (all its tiles of one vocabulary
+// range run together); with few row tiles each XCD owns a contiguous range of
+// vocabulary tiles.
+__device__ __forceinline__ bool map_job(int bid, int nvt, int nrt, int split_rows, int& rt, int& vt) {
+  const int xcd = bid & 7, local = bid >> 3;
+  if (split_rows) {
+    const int lo = (int)((long long)xcd * nrt / 8), hi = (int)((long long)(xcd + 1) * nrt / 8);
+    const int nr = hi - lo;
+    if (nr <= 0 || local >= nr * nvt) return false;
+    vt = local / nr;
+    rt = lo + (local - vt * nr);
+  } else {
+    const int lo = (int)((long long)xcd * nvt / 8), hi = (int)((long long)(xcd + 1) * nvt / 8);
+    const int nv = hi - lo;
+    if (nv <= 0 || local >= nv * nrt) return false;
+    const int q = local / nrt;
+    vt = lo + q;
+    rt = local - q * nrt;
+  }
+  return true;
+}
+
+// hidden-state chunk c (TR rows x KC elements) -> registers, zero beyond d or
+// for padding rows (offset -1)
+template <int TR, int KC, int NT, int XPT>
+__device__ __forceinline__ void load_x_chunk(uint4 (&xr)[XPT], const uint16_t* __restrict__ hidden,
+                                             const long long* xoff, int c, int tid, int d) {
+  constexpr int XP = TR * (KC / 8);
+#pragma unroll
+  for (int j = 0; j < XPT; ++j) {
+    const int q = tid + j * NT;
+    if (XP % NT == 0 || q < XP) {
+      const int row = q / (KC / 8), c8 = q - row * (KC / 8);
+      const int k = c * KC + c8 * 8;
+      const long long off = xoff[row];
+      xr[j] = (off >= 0 && k < d) ? *reinterpret_cast<const uint4*>(hidden + off + k) : make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+}
+
+template <int TR, int KC, int KCP, int NT, int XPT>
+__device__ __forceinline__ void store_x_chunk(uint16_t (*xsb)[KCP], const uint4 (&xr)[XPT], int tid) {
+  constexpr int XP = TR * (KC / 8);
+#pragma unroll
+  for (int j = 0; j < XPT; ++j) {
+    const int q = tid + j * NT;
+    if (XP % NT == 0 || q < XP) {
+      const int row = q / (KC / 8), c8 = q - row * (KC / 8);
+      *reinterpret_cast<uint4*>(&xsb[row][c8 * 8]) = xr[j];
+    }
+  }
+}
+
+// this lane's W_U operand for chunk c: KS k-steps x MV 16-row blocks
+template <int MV, int KS>
+__device__ __forceinline__ void load_a_chunk(uint4 (&dst)[KS][MV], const uint16_t* __restrict__ w_u,
+                                             const long long (&aoff)[MV], int c, int kl, int d) {
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const int k = c * 64 + s * 32;
+#pragma unroll
+    for (int mv = 0; mv < MV; ++mv)
+      dst[s][mv] = (k + kl < d) ? *reinterpret_cast<const uint4*>(w_u + aoff[mv] + k) : make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+// Workgroup tile: TR = 16*NB projected rows x up to 16*MV*NW vocabulary rows,
+// over the full hidden dimension. Each wave owns 16*MV consecutive W_U rows;
+// its W_U operand goes straight from memory into registers (every W_U element
+// is used by exactly one wave) with one 64-element chunk of prefetch, while
+// the TR rows of hidden states, shared by all waves, are staged through a
+// double-buffered LDS tile. v_mfma_f32_16x16x32_bf16 computes 16 vocab x 16
+// rows; W_U is the A operand, so accumulator lane l holds, for row (l & 15)
+// of its 16-row block, the logits of vocabulary entries 4*(l >> 4) + 0..3.
+// The epilogue turns each lane's logits into a softmax state, merges the four
+// lanes of a row and then the waves, and writes one 16-byte partial state per
+// (row, vocab tile).
+template <int NW, int MV, int NB>
+__global__ __launch_bounds__(NW * 64) void k_proj_bf16(
+    const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
+    int nvt, int nrt, int split_rows) {
+  constexpr int TR = 16 * NB;
+  constexpr int KC = 64;           // k elements per chunk
+  constexpr int KS = KC / 32;      // MFMA k-steps per chunk
+  constexpr int KCP = KC + 8;      // padded LDS row length (elements)
+  constexpr int NT = NW * 64;
+  constexpr int XP = TR * (KC / 8);           // 16-byte pieces per hidden chunk
+  constexpr int XPT = (XP + NT - 1) / NT;     // pieces per thread
+
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2][TR][KCP];
+  __shared__ long long xoff[TR];
+  __shared__ float4 red[NW][TR];
+
+  int rt, vt;
+  if (!map_job(blockIdx.x, nvt, nrt, split_rows, rt, vt)) return;
+  const int R = *n_ptr * K;
+  const int r0 = rt * TR;
+  if (r0 >= R) return;
+  const int vb = (int)((long long)vt * V / nvt);
+  const int ve = (int)((long long)(vt + 1) * V / nvt);
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+
+  for (int t = tid; t < TR; t += NT) {
+    const int r = r0 + t;
+    long long off = -1;
+    if (r < R) {
+      const int p = r / K, l = r - p * K;
+      const int pos = rows[p];
+      const int b = pos / L, i = pos - b * L;
+      off = (((long long)l * B + b) * L + i) * (long long)d;
+    }
+    xoff[t] = off;
+  }
+  __syncthreads();
+
+  const int vw = vb + wid * 16 * MV;
+  const int kl = (lane >> 4) * 8;  // this lane's k offset inside a 32-wide k-step
+  long long aoff[MV];               // element offset of this lane's W_U row, per 16-row block
+#pragma unroll
+  for (int mv = 0; mv < MV; ++mv) aoff[mv] = (long long)min(vw + mv * 16 + (lane & 15), ve - 1) * d + kl;
+
+  f32x4 acc[MV][NB];
+#pragma unroll
+  for (int mv = 0; mv < MV; ++mv)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mv][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  uint4 a_cur[KS][MV], a_nxt[KS][MV];
+  uint4 xr[XPT];
+  const int nch = (d + KC - 1) / KC;
+
+  load_x_chunk<TR, KC, NT, XPT>(xr, hidden, xoff, 0, tid, d);
+  load_a_chunk<MV, KS>(a_cur, w_u, aoff, 0, kl, d);
+  store_x_chunk<TR, KC, KCP, NT, XPT>(xs[0], xr, tid);
+  __syncthreads();
+
+  for (int c = 0; c < nch; ++c) {
+    const int buf = c & 1;
+    const bool more = (c + 1) < nch;
+    if (more) {
+      load_x_chunk<TR, KC, NT, XPT>(xr, hidden, xoff, c + 1, tid, d);
+      load_a_chunk<MV, KS>(a_nxt, w_u, aoff, c + 1, kl, d);
+    }
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const uint4 bq = *reinterpret_cast<const uint4*>(&xs[buf][nb * 16 + (lane & 15)][s * 32 + kl]);
+        const bf16x8 bv = __builtin_bit_cast(bf16x8, bq);
+#pragma unroll
+        for (int mv = 0; mv < MV; ++mv)
+          acc[mv][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a_cur[s][mv]), bv,
+                                                                 acc[mv][nb], 0, 0, 0);
+      }
+    }
+    if (more) store_x_chunk<TR, KC, KCP, NT, XPT>(xs[buf ^ 1], xr, tid);
+    __syncthreads();
+    if (more) {
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+#pragma unroll
+        for (int mv = 0; mv < MV; ++mv) a_cur[s][mv] = a_nxt[s][mv];
+    }
+  }
+
+  // epilogue: softmax state per projected row
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    float z[MV * 4];
+    int vi[MV * 4];
+    bool ok[MV * 4];
+#pragma unroll
+    for (int mv = 0; mv < MV; ++mv)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int v = vw + mv * 16 + (lane >> 4) * 4 + e;
+        z[mv * 4 + e] = acc[mv][nb][e];
+        vi[mv * 4 + e] = v;
+        ok[mv * 4 + e] = v < ve;
+      }
+    Soft st = soft_from_values(z, vi, ok);
+    st = soft_merge(st, soft_shfl_xor(st, 16));
+    st = soft_merge(st, soft_shfl_xor(st, 32));
+    if (lane < 16) red[wid][nb * 16 + lane] = soft_pack(st);
+  }
+  __syncthreads();
+  for (int t = tid; t < TR; t += NT) {
+    const int r = r0 + t;
+    if (r < R) {
+      Soft s = soft_unpack(red[0][t]);
+#pragma unroll
+      for (int w = 1; w < NW; ++w) s = soft_merge(s, soft_unpack(red[w][t]));
+      partials[(long long)r * nvt + vt] = soft_pack(s);
+    }
+  }
+}
+
+// ------------------------------------------------------ K1 projection f32 --
+
+// fp32 inputs: 64 vocabulary rows (one per lane) x 16 projected rows (four
+// per wave) per workgroup, fp32 FMA on the vector ALU through LDS tiles.
+__global__ __launch_bounds__(256) void k_proj_f32(const float* __restrict__ hidden, const float* __restrict__ w_u,
+                                                  const int32_t* __restrict__ rows,
+                                                  const int32_t* __restrict__ n_ptr, float4* __restrict__ partials,
+                                                  int K, int B, int L, int d, int V, int nvt) {
+  __shared__ float ws[64][33];
+  __shared__ float xsm[16][33];
+  __shared__ long long xoff[16];
+  const int vt = blockIdx.x % nvt, rt = blockIdx.x / nvt;
+  const int R = *n_ptr * K;
+  const int r0 = rt * 16;
+  if (r0 >= R) return;
+  const int vb = (int)((long long)vt * V / nvt);
+  const int ve = (int)((long long)(vt + 1) * V / nvt);
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  if (tid < 16) {
+    const int r = r0 + tid;
+    long long off = -1;
+    if (r < R) {
+      const int p = r / K, l = r - p * K;
+      const int pos = rows[p];
+      const int b = pos / L, i = pos - b * L;
+      off = (((long long)l * B + b) * L + i) * (long long)d;
+    }
+    xoff[tid] = off;
+  }
+  __syncthreads();
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < d; k0 += 32) {
+    for (int q = tid; q < 64 * 32; q += 256) {
+      const int row = q >> 5, kk = q & 31;
+      const int v = vb + row;
+      ws[row][kk] = (v < ve && k0 + kk < d) ? w_u[(long long)v * d + k0 + kk] : 0.f;
+    }
+    for (int q = tid; q < 16 * 32; q += 256) {
+      const int row = q >> 5, kk = q & 31;
+      const long long off = xoff[row];
+      xsm[row][kk] = (off >= 0 && k0 + kk < d) ? hidden[off + k0 + kk] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int kk = 0; kk < 32; ++kk) {
+      const float wv = ws[lane][kk];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = fmaf(wv, xsm[wid * 4 + j][kk], acc[j]);
+    }
+    __syncthreads();
+  }
+  const int v = vb + lane;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float z[1] = {acc[j]};
+    int vi[1] = {v};
+    bool ok[1] = {v < ve};
+    Soft st = soft_from_values(z, vi, ok);
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) st = soft_merge(st, soft_shfl_xor(st, m));
+    const int r = r0 + wid * 4 + j;
+    if (lane == 0 && r < R) partials[(long long)r * nvt + vt] = soft_pack(st);
+  }
+}
+
+// ------------------------------------------------------ scoring (Eq. 2-5) --
+
+__device__ __forceinline__ float stability_score(int k_i, float r_i, int k_max, float w) {
+  return fmaf(-w, r_i, (float)min(k_i, k_max));
+}
+
+__device__ __forceinline__ unsigned route_flags(float c, float s, float theta_h, float theta_c, float theta_s) {
+  const bool high = c >= theta_h;
+  const bool stab = (c >= theta_c) && (c < theta_h) && (s >= theta_s);
+  return (high || stab ? kFlagCandidate : 0u) | (high ? kFlagHigh : 0u) | (stab ? kFlagStable : 0u);
+}
+
+struct ScoreArgs {
+  int K, B, L;
+  float theta_h, theta_c, theta_s, w;
+  int k_max;
+  int32_t* token;
+  float* entropy;
+  float* confidence;
+  int32_t* persistence;
+  float* drop;
+  float* stability;
+  uint8_t* flags;
+  int32_t* layer_argmax;
+  float* layer_conf;
+  float* layer_entropy;
+};
+
+// One wave per masked position: merge the vocab-tile states of each of its K
+// rows (lane-strided in tile order, then a fixed butterfly), giving every
+// lane the layer's argmax, top probability and entropy; lane l keeps layer
+// l. Persistence, drop and stability are then evaluated across lanes.
+__global__ __launch_bounds__(256) void k_reduce_score(const float4* __restrict__ partials,
+                                                       const int32_t* __restrict__ rows,
+                                                       const int32_t* __restrict__ n_ptr, int nvt, ScoreArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int p = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (p >= *n_ptr) return;
+  const int pos = rows[p];
+  const int b = pos / a.L, i = pos - b * a.L;
+  int my_y = -1;
+  float my_c = 0.f, my_h = 0.f;
+  for (int l = 0; l < a.K; ++l) {
+    const float4* src = partials + ((long long)p * a.K + l) * nvt;
+    Soft s = soft_empty();
+    for (int t = lane; t < nvt; t += 64) s = soft_merge(s, soft_unpack(src[t]));
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) s = soft_merge(s, soft_shfl_xor(s, m));
+    const float c = 1.0f / s.S;
+    const float h = fmaxf(logf(s.S) - s.T / s.S, 0.0f);
+    const float h_out = (s.S != s.S) ? s.S : h;   // keep NaN visible
+    const int y = (s.idx == INT_MAX) ? -1 : s.idx;
+    if (lane == l) {
+      my_y = y;
+      my_c = c;
+      my_h = h_out;
+    }
+  }
+  const int yK = __shfl(my_y, a.K - 1);
+  const float cK = __shfl(my_c, a.K - 1);
+  const float hK = __shfl(my_h, a.K - 1);
+  // Eq. 2: agreement suffix ending at the final layer
+  const unsigned long long dis = __ballot(lane < a.K && my_y != yK);
+  const int last_dis = dis ? 63 - __clzll(dis) : -1;
+  const int k_i = a.K - 1 - last_dis;
+  // Eq. 3: inside the suffix the final token is each layer's argmax, so its
+  // probability there is that layer's top probability
+  float pk = (lane >= a.K - k_i && lane < a.K) ? my_c : -INFINITY;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) pk = fmaxf(pk, __shfl_xor(pk, m));
+  const float r_i = pk - cK;
+  const float s_i = stability_score(k_i, r_i, a.k_max, a.w);
+  const unsigned fl = route_flags(cK, s_i, a.theta_h, a.theta_c, a.theta_s);
+  const long long o = (long long)b * a.L + i;
+  if (lane == 0) {
+    a.token[o] = yK;
+    a.entropy[o] = hK;
+    a.confidence[o] = cK;
+    a.persistence[o] = k_i;
+    a.drop[o] = r_i;
+    a.stability[o] = s_i;
+    a.flags[o] = (uint8_t)fl;
+  }
+  if (a.layer_argmax && lane < a.K) {
+    const long long ol = ((long long)lane * a.B + b) * a.L + i;
+    a.layer_argmax[ol] = my_y;
+    a.layer_conf[ol] = my_c;
+    a.layer_entropy[ol] = my_h;
+  }
+}
+
+// Scoring from caller-supplied per-layer statistics, one thread per canvas
+// position (same formulas as k_reduce_score, evaluated sequentially).
+__global__ __launch_bounds__(256) void k_gate_score(const uint8_t* __restrict__ mask,
+                                                     const int32_t* __restrict__ l_y,
+                                                     const float* __restrict__ l_c,
+                                                     const float* __restrict__ l_h, ScoreArgs a) {
+  const long long BL = (long long)a.B * a.L;
+  const long long o = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (o >= BL || mask[o] == 0) return;
+  const int yK = l_y[(long long)(a.K - 1) * BL + o];
+  const float cK = l_c[(long long)(a.K - 1) * BL + o];
+  const float hK = l_h[(long long)(a.K - 1) * BL + o];
+  int k_i = 1;
+  float pk = cK;
+  for (int l = a.K - 2; l >= 0; --l) {
+    if (l_y[(long long)l * BL + o] != yK) break;
+    ++k_i;
+    pk = fmaxf(pk, l_c[(long long)l * BL + o]);
+  }
+  const float r_i = pk - cK;
+  const float s_i = stability_score(k_i, r_i, a.k_max, a.w);
+  a.token[o] = yK;
+  a.entropy[o] = hK;
+  a.confidence[o] = cK;
+  a.persistence[o] = k_i;
+  a.drop[o] = r_i;
+  a.stability[o] = s_i;
+  a.flags[o] = (uint8_t)route_flags(cK, s_i, a.theta_h, a.theta_c, a.theta_s);
+}
+
+// --------------------------------------------------- commitment (Sec. 3.2) --
+
+constexpr int kCommitThreads = 1024;
+
+// exclusive prefix sum over the workgroup in thread order (fixed tree order);
+// `total` receives the sum of all values
+template <typename T>
+__device__ __forceinline__ T block_exclusive_scan(T v, T* sh, T& total) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  T x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const T y = __shfl_up(x, o);
+    if (lane >= o) x = x + y;
+  }
+  if (lane == 63) sh[wid] = x;
+  __syncthreads();
+  if (wid == 0) {
+    T s = (lane < nw) ? sh[lane] : T(0);
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const T y = __shfl_up(s, o);
+      if (lane >= o) s = s + y;
+    }
+    if (lane < nw) sh[32 + lane] = s;   // inclusive over waves
+  }
+  __syncthreads();
+  const T wave_before = (wid == 0) ? T(0) : sh[32 + wid - 1];
+  total = sh[32 + nw - 1];
+  const T res = wave_before + x - v;
+  __syncthreads();
+  return res;
+}
+
+struct CommitArgs {
+  int B, L;
+  float beta;
+  int window;
+  uint8_t* commit;
+  int32_t* token;
+  float* entropy;
+  float* confidence;
+  int32_t* persistence;
+  float* drop;
+  float* stability;
+  uint8_t* flags;
+  float* upstream_entropy;
+  int32_t* n_commit;
+};
+
+// One workgroup per sequence. N_i = entropy summed over earlier masked
+// non-candidates; a candidate is committed iff N_i <= beta, which is exactly
+// the left-to-right construction of the paper (every earlier candidate of an
+// accepted position is accepted, so the positions left out before it are the
+// non-candidates; a rejected candidate's sum only grows). E_i (reported) is
+// the entropy over earlier masked positions not committed. Without any
+// commit, the most confident of the first `window` masked positions is
+// committed (lowest index on ties; NaN confidences never win).
+__global__ __launch_bounds__(kCommitThreads) void k_commit(const uint8_t* __restrict__ mask, CommitArgs a) {
+  __shared__ float shf[64];
+  __shared__ int shi[64];
+  __shared__ float red_c[16];
+  __shared__ int red_i[16];
+  const int b = blockIdx.x;
+  const long long base = (long long)b * a.L;
+  float carryN = 0.f, carryE = 0.f;
+  int carryM = 0, ncommit = 0;
+  float best_c = -INFINITY;
+  int best_i = INT_MAX;
+  for (int c0 = 0; c0 < a.L; c0 += blockDim.x) {
+    const int i = c0 + threadIdx.x;
+    const bool in = i < a.L;
+    const bool masked = in && mask[base + i] != 0;
+    const unsigned fl = masked ? a.flags[base + i] : 0u;
+    const bool cand = (fl & kFlagCandidate) != 0;
+    const float H = masked ? a.entropy[base + i] : 0.f;
+    float totN, totE;
+    int totM;
+    const float N_i = carryN + block_exclusive_scan<float>((masked && !cand) ? H : 0.f, shf, totN);
+    const bool com = masked && cand && (N_i <= a.beta);
+    const float E_i = carryE + block_exclusive_scan<float>((masked && !com) ? H : 0.f, shf, totE);
+    const int rank = carryM + block_exclusive_scan<int>(masked ? 1 : 0, shi, totM);
+    int ncom_chunk;
+    (void)block_exclusive_scan<int>(com ? 1 : 0, shi, ncom_chunk);
+    if (in) {
+      const long long o = base + i;
+      if (masked) {
+        a.commit[o] = com ? 1 : 0;
+        a.flags[o] = (uint8_t)(fl | (com ? kFlagCommitted : 0u));
+        a.upstream_entropy[o] = E_i;
+        if (rank < a.window) {
+          float cv = a.confidence[o];
+          cv = (cv != cv) ? -INFINITY : cv;
+          if (cv > best_c || (cv == best_c && i < best_i)) {
+            best_c = cv;
+            best_i = i;
+          }
+        }
+      } else {
+        a.commit[o] = 0;
+        a.token[o] = -1;
+        a.entropy[o] = 0.f;
+        a.confidence[o] = 0.f;
+        a.persistence[o] = 0;
+        a.drop[o] = 0.f;
+        a.stability[o] = 0.f;
+        a.flags[o] = 0;
+        a.upstream_entropy[o] = 0.f;
+      }
+    }
+    carryN += totN;
+    carryE += totE;
+    carryM += totM;
+    ncommit += ncom_chunk;
+  }
+  if (ncommit == 0 && carryM > 0) {
+    // workgroup argmax of (confidence, -index) over the window
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const float oc = __shfl_xor(best_c, m);
+      const int oi = __shfl_xor(best_i, m);
+      if (oc > best_c || (oc == best_c && oi < best_i)) {
+        best_c = oc;
+        best_i = oi;
+      }
+    }
+    if (lane == 0) {
+      red_c[wid] = best_c;
+      red_i[wid] = best_i;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float bc = red_c[0];
+      int bi = red_i[0];
+      for (int w = 1; w < nw; ++w)
+        if (red_c[w] > bc || (red_c[w] == bc && red_i[w] < bi)) {
+          bc = red_c[w];
+          bi = red_i[w];
+        }
+      if (bi != INT_MAX) {   // the window always holds a masked position here
+        const long long o = base + bi;
+        a.commit[o] = 1;
+        a.flags[o] = (uint8_t)(a.flags[o] | kFlagCommitted | kFlagFallback);
+        ncommit = 1;
+      }
+    }
+  }
+  if (threadIdx.x == 0) a.n_commit[b] = ncommit;
+}
+
+ScoreArgs score_args(const Launch& a) {
+  ScoreArgs s;
+  s.K = a.K;
+  s.B = a.B;
+  s.L = a.L;
+  s.theta_h = a.theta_h;
+  s.theta_c = a.theta_c;
+  s.theta_s = a.theta_s;
+  s.w = a.w;
+  s.k_max = a.k_max;
+  s.token = a.token;
+  s.entropy = a.entropy;
+  s.confidence = a.confidence;
+  s.persistence = a.persistence;
+  s.drop = a.drop;
+  s.stability = a.stability;
+  s.flags = a.flags;
+  s.layer_argmax = a.layer_argmax;
+  s.layer_conf = a.layer_conf;
+  s.layer_entropy = a.layer_entropy;
+  return s;
+}
+
+CommitArgs commit_args(const Launch& a) {
+  CommitArgs c;
+  c.B = a.B;
+  c.L = a.L;
+  c.beta = a.beta;
+  c.window = a.window;
+  c.commit = a.commit;
+  c.token = a.token;
+  c.entropy = a.entropy;
+  c.confidence = a.confidence;
+  c.persistence = a.persistence;
+  c.drop = a.drop;
+  c.stability = a.stability;
+  c.flags = a.flags;
+  c.upstream_entropy = a.upstream_entropy;
+  c.n_commit = a.n_commit;
+  return c;
+}
+
+template <int NW, int MV, int NB>
+void launch_proj_bf16(const Launch& a, hipStream_t s) {
+  const ProjPlan& p = a.plan;
+  hipLaunchKernelGGL((k_proj_bf16<NW, MV, NB>), dim3(p.grid), dim3(NW * 64), 0, s,
+                     static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
+                     a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows);
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ host --
+
+ProjPlan plan_projection(int dtype, long long rows_cap, int V) {
+  ProjPlan p{};
+  if (rows_cap < 1) rows_cap = 1;
+  if (dtype == 1) {   // fp32
+    p.variant = PROJ_F32;
+    p.rows_per_tile = 16;
+    p.vocab_cap = 64;
+    p.nvt = (V + 63) / 64;
+    p.nrt = (int)((rows_cap + 15) / 16);
+    p.split_rows = 0;
+    p.per_xcd = 0;
+    p.grid = p.nvt * p.nrt;
+    return p;
+  }
+  if (rows_cap <= 64) {
+    p.variant = rows_cap <= 32 ? PROJ_BF16_R32 : PROJ_BF16_R64;
+    p.rows_per_tile = rows_cap <= 32 ? 32 : 64;
+    p.vocab_cap = 8 * 64;
+    // every CU streams an equal share of W_U: a multiple of 256 tiles
+    int nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
+    nvt = ((nvt + 255) / 256) * 256;
+    p.nvt = nvt < V ? nvt : V;
+  } else {
+    p.variant = PROJ_BF16_R128;
+    p.rows_per_tile = 128;
+    p.vocab_cap = 4 * 64;
+    p.nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
+  }
+  p.nrt = (int)((rows_cap + p.rows_per_tile - 1) / p.rows_per_tile);
+  p.split_rows = p.nrt >= 8 ? 1 : 0;
+  p.per_xcd = p.split_rows ? ((p.nrt + 7) / 8) * p.nvt : ((p.nvt + 7) / 8) * p.nrt;
+  p.grid = 8 * p.per_xcd;
+  return p;
+}
+
+hipError_t launch_compact(const Launch& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, a.mask, a.B * a.L, a.max_masked, a.rows, a.n_masked,
+                     a.dev_status, a.user_status);
+  return hipGetLastError();
+}
+
+hipError_t launch_projection(const Launch& a, hipStream_t s) {
+  if (a.max_masked <= 0) return hipSuccess;
+  switch (a.plan.variant) {
+    case PROJ_BF16_R32: launch_proj_bf16<8, 4, 2>(a, s); break;
+    case PROJ_BF16_R64: launch_proj_bf16<8, 4, 4>(a, s); break;
+    case PROJ_BF16_R128: launch_proj_bf16<4, 4, 8>(a, s); break;
+    case PROJ_F32:
+      hipLaunchKernelGGL(k_proj_f32, dim3(a.plan.grid), dim3(256), 0, s, static_cast<const float*>(a.hidden),
+                         static_cast<const float*>(a.w_u), a.rows, a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V,
+                         a.plan.nvt);
+      break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_score(const Launch& a, hipStream_t s) {
+  if (a.max_masked <= 0) return hipSuccess;
+  const int per_wg = 4;
+  hipLaunchKernelGGL(k_reduce_score, dim3((a.max_masked + per_wg - 1) / per_wg), dim3(64 * per_wg), 0, s,
+                     a.partials, a.rows, a.n_masked, a.plan.nvt, score_args(a));
+  return hipGetLastError();
+}
+
+hipError_t launch_commit(const Launch& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_commit, dim3(a.B), dim3(kCommitThreads), 0, s, a.mask, commit_args(a));
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_commit(const Launch& a, const int32_t* l_y, const float* l_c, const float* l_h,
+                              hipStream_t s) {
+  const long long BL = (long long)a.B * a.L;
+  hipLaunchKernelGGL(k_gate_score, dim3((unsigned)((BL + 255) / 256)), dim3(256), 0, s, a.mask, l_y, l_c, l_h,
+                     score_args(a));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_commit, dim3(a.B), dim3(kCommitThreads), 0, s, a.mask, commit_args(a));
+  return hipGetLastError();
+}
+
+}  // namespace rpd

@@ -1,0 +1,68 @@
+// Internal interface between the C ABI (rpd_api.cpp) and the gfx950 kernels
+// (rpd_kernels.hip). Not installed; no torch or HIP types beyond hipStream_t.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rpd {
+
+// Projection kernel shapes. A "row" is one (masked position, layer) pair:
+// row r = p*K + l for compacted masked position p. A "vocab tile" is a
+// contiguous range of W_U rows; tile t covers [t*V/NVT, (t+1)*V/NVT).
+enum ProjVariant {
+  PROJ_BF16_R32 = 0,   // small row count: 32 rows per tile, 8 waves x 64 vocab
+  PROJ_BF16_R64 = 1,   // 64 rows per tile, 8 waves x 64 vocab
+  PROJ_BF16_R128 = 2,  // 128 rows per tile, 4 waves x 64 vocab (large row counts)
+  PROJ_F32 = 3,        // fp32 inputs: vector ALU, 16 rows x 64 vocab
+};
+
+struct ProjPlan {
+  ProjVariant variant;
+  int rows_per_tile;   // TR
+  int vocab_cap;       // max vocab rows one tile can hold
+  int nvt;             // number of vocab tiles
+  int nrt;             // number of row tiles (for the row bound)
+  int per_xcd;         // workgroups per XCD slot in the launch
+  int split_rows;      // 1: XCDs own row tiles; 0: XCDs own vocab tiles
+  int grid;            // workgroups launched
+};
+
+// the shape plan for `rows_cap` rows (K * max masked positions)
+ProjPlan plan_projection(int dtype, long long rows_cap, int V);
+
+struct Launch {
+  int K, B, L, d, V;
+  const void* hidden;
+  const void* w_u;
+  const uint8_t* mask;
+  int max_masked;        // bound used for the launches (>= 0)
+  // workspace pieces
+  int32_t* n_masked;     // [1] device count (clamped to max_masked)
+  int32_t* dev_status;   // [1] internal status word
+  int32_t* rows;         // [max_masked] compacted b*L+i
+  float4* partials;      // [K*max_masked][nvt]
+  ProjPlan plan;
+  // params
+  float theta_h, theta_c, theta_s, w, beta;
+  int k_max, window;
+  // outputs
+  uint8_t* commit; int32_t* token; float* entropy; float* confidence;
+  int32_t* persistence; float* drop; float* stability; uint8_t* flags;
+  float* upstream_entropy; int32_t* n_commit;
+  int32_t* layer_argmax; float* layer_conf; float* layer_entropy;
+  int32_t* user_status;
+};
+
+// enqueue, in this order: compaction, projection, reduction + scoring,
+// commitment (the last three use a.plan and a.max_masked)
+hipError_t launch_compact(const Launch& a, hipStream_t s);
+hipError_t launch_projection(const Launch& a, hipStream_t s);
+hipError_t launch_reduce_score(const Launch& a, hipStream_t s);
+hipError_t launch_commit(const Launch& a, hipStream_t s);
+
+// scoring + commitment from caller-supplied per-layer statistics
+hipError_t launch_gate_commit(const Launch& a, const int32_t* layer_argmax, const float* layer_conf,
+                              const float* layer_entropy, hipStream_t s);
+
+}  // namespace rpd

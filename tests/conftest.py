@@ -11,3 +11,13 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: full-size case, several seconds or more")
+
+
+@pytest.fixture(scope="session", autouse=True)
+def _library_built():
+    """Build librpd.so once if it is missing (tests load what is built)."""
+    lib = os.path.join(ROOT, "paper_2609_36452_amd", "librpd.so")
+    if not os.path.exists(lib):
+        from paper_2609_36452_amd.build import build
+        build()
+    yield

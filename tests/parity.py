@@ -1,0 +1,189 @@
+"""Element-by-element comparison of the HIP path with the fp64 oracle.
+
+Contract (floating point): per masked position and per layer, entropy within
+2e-3 nats and top probability within 1e-3 (bf16 inputs, fp32 accumulation).
+Integer results (argmax, token, persistence, candidacy, commit, counts) must
+be bit-exact, except where the exact answer is decided by a margin smaller
+than the arithmetic can resolve; such positions are reported by class and not
+counted as mismatches:
+
+1. argmax near-tie: oracle top-2 logit gap below ``4 (d+1) u max(A_1, A_2)``,
+   ``A_v = sum_k |W_U[v,k] x_k|``, u = 2^-24 -- twice the worst-case bound of
+   fp32 accumulation in any order, leaving room for the matrix cores'
+   internal rounding;
+2. threshold near-tie: confidence within 1e-3 of theta_h or theta_c;
+3. stability near-tie: oracle S_i within w * 2e-3 of theta_s (r_i is a
+   difference of two probabilities, each within 1e-3);
+4. budget near-tie: oracle prefix N_i within 1e-4 + sum of the entropy errors
+   over the earlier masked non-candidates (+ the entropy of earlier positions
+   whose candidacy was itself excused) of beta;
+5. fallback near-tie: the two best confidences of the fallback window within
+   2e-3, or a sequence whose fallback decision follows from an excused
+   difference above.
+"""
+from __future__ import annotations
+
+from collections import Counter
+
+import numpy as np
+
+ENTROPY_TOL = 2e-3
+CONF_TOL = 1e-3
+U = 2.0 ** -24
+
+F_CAND, F_HIGH, F_STAB, F_COMMIT, F_FALLBACK = 1, 2, 4, 8, 16
+
+
+def gap_tol(d: int, absbound):
+    return 4.0 * (d + 1) * U * np.asarray(absbound)
+
+
+class Report:
+    def __init__(self):
+        self.fail: list[str] = []
+        self.excused = Counter()
+        self.checked = Counter()
+
+    def bad(self, msg: str):
+        if len(self.fail) < 40:
+            self.fail.append(msg)
+        else:
+            self.fail.append("...")
+
+    def ok(self) -> bool:
+        return not self.fail
+
+    def summary(self) -> str:
+        return f"checked={dict(self.checked)} excused={dict(self.excused)} failures={self.fail[:20]}"
+
+
+def compare(g: dict, o: dict, mask: np.ndarray, P, d: int, layer: bool = True) -> Report:
+    """g: GPU outputs as numpy; o: oracle outputs (oracle.score_commit)."""
+    rep = Report()
+    B, L = mask.shape
+    K = o["layer_argmax"].shape[0]
+    m = mask != 0
+    # unmasked sentinels
+    for name, val in (("commit", 0), ("token", -1), ("persistence", 0), ("flags", 0), ("entropy", 0.0),
+                      ("confidence", 0.0), ("drop", 0.0), ("stability", 0.0), ("upstream_entropy", 0.0)):
+        if np.any(g[name][~m] != val):
+            rep.bad(f"unmasked sentinel {name}")
+    tie_any = np.zeros((B, L), bool)      # argmax near-tie at some layer
+    # per-layer statistics
+    if layer:
+        for l in range(K):
+            gy, oy = g["layer_argmax"][l], o["layer_argmax"][l]
+            gc, oc = g["layer_conf"][l], o["layer_conf"][l]
+            gh, oh = g["layer_entropy"][l], o["layer_entropy"][l]
+            tie = o["layer_gap"][l] < gap_tol(d, o["layer_absbound"][l])
+            tie_any |= tie & m
+            for b, i in zip(*np.nonzero(m)):
+                rep.checked["layer"] += 1
+                if np.isnan(oh[b, i]):
+                    if not (np.isnan(gh[b, i]) and np.isnan(gc[b, i])):
+                        rep.bad(f"NaN row not NaN on GPU at l={l} b={b} i={i}")
+                    continue
+                if abs(gh[b, i] - oh[b, i]) > ENTROPY_TOL:
+                    rep.bad(f"entropy l={l} b={b} i={i}: gpu {gh[b, i]:.6g} oracle {oh[b, i]:.6g}")
+                if abs(gc[b, i] - oc[b, i]) > CONF_TOL:
+                    rep.bad(f"conf l={l} b={b} i={i}: gpu {gc[b, i]:.6g} oracle {oc[b, i]:.6g}")
+                if gy[b, i] != oy[b, i]:
+                    if tie[b, i]:
+                        rep.excused["argmax_tie"] += 1
+                    else:
+                        rep.bad(f"argmax l={l} b={b} i={i}: gpu {gy[b, i]} oracle {oy[b, i]} "
+                                f"gap {o['layer_gap'][l][b, i]:.3g}")
+    else:
+        tie_any |= (o["layer_gap"] < gap_tol(d, o["layer_absbound"])).any(0) & m
+    nan_pos = np.isnan(o["entropy"]) & m
+    # per-position scoring
+    cand_excused = np.zeros((B, L), bool)
+    for b, i in zip(*np.nonzero(m)):
+        rep.checked["position"] += 1
+        if nan_pos[b, i]:
+            if g["flags"][b, i] & F_CAND:
+                rep.bad(f"NaN position b={b} i={i} became a candidate")
+            continue
+        for name, tol in (("entropy", ENTROPY_TOL), ("confidence", CONF_TOL)):
+            if abs(g[name][b, i] - o[name][b, i]) > tol:
+                rep.bad(f"{name} b={b} i={i}: gpu {g[name][b, i]:.6g} oracle {o[name][b, i]:.6g}")
+        if g["token"][b, i] != o["token"][b, i] and not tie_any[b, i]:
+            rep.bad(f"token b={b} i={i}: gpu {g['token'][b, i]} oracle {o['token'][b, i]}")
+        same_k = g["persistence"][b, i] == o["persistence"][b, i]
+        if not same_k:
+            if tie_any[b, i]:
+                rep.excused["persistence_tie"] += 1
+            else:
+                rep.bad(f"persistence b={b} i={i}: gpu {g['persistence'][b, i]} oracle {o['persistence'][b, i]}")
+        elif abs(g["drop"][b, i] - o["drop"][b, i]) > 2 * CONF_TOL or \
+                abs(g["stability"][b, i] - o["stability"][b, i]) > P.w * 2 * CONF_TOL + 1e-6:
+            rep.bad(f"drop/stability b={b} i={i}: gpu {g['drop'][b, i]:.6g}/{g['stability'][b, i]:.6g} "
+                    f"oracle {o['drop'][b, i]:.6g}/{o['stability'][b, i]:.6g}")
+        gf, of = int(g["flags"][b, i]) & 7, int(o["flags"][b, i]) & 7
+        if gf != of:
+            c = o["confidence"][b, i]
+            if tie_any[b, i]:
+                why = "cand_argmax_tie"
+            elif abs(c - P.theta_h) <= CONF_TOL or abs(c - P.theta_c) <= CONF_TOL:
+                why = "threshold_tie"
+            elif abs(o["stability"][b, i] - P.theta_s) <= P.w * 2 * CONF_TOL:
+                why = "stability_tie"
+            else:
+                why = None
+            if why is None:
+                rep.bad(f"route flags b={b} i={i}: gpu {gf} oracle {of} c={c:.6g} S={o['stability'][b, i]:.6g}")
+            else:
+                rep.excused[why] += 1
+                if (gf ^ of) & F_CAND:
+                    cand_excused[b, i] = True
+    # commitment per sequence
+    for b in range(B):
+        idx = np.nonzero(m[b])[0]
+        if idx.size == 0:
+            if g["n_commit"][b] != 0:
+                rep.bad(f"n_commit b={b} with no masked position")
+            continue
+        ocand = (o["flags"][b, idx] & F_CAND) > 0
+        dH = np.abs(np.nan_to_num(g["entropy"][b, idx] - o["entropy"][b, idx]))
+        slack = 1e-4 + np.concatenate([[0.0], np.cumsum(np.where(ocand, 0.0, dH))[:-1]])
+        slack = slack + np.concatenate([[0.0], np.cumsum(np.where(cand_excused[b, idx],
+                                                                  np.nan_to_num(o["entropy"][b, idx]), 0.0))[:-1]])
+        N = o["budget_prefix"][b, idx]
+        budget_tie = np.abs(N - P.beta) <= slack
+        gcm = g["commit"][b, idx] != 0
+        ocm = o["commit"][b, idx] != 0
+        gfb = (g["flags"][b, idx] & F_FALLBACK) > 0
+        ofb = (o["flags"][b, idx] & F_FALLBACK) > 0
+        excusable_seq = bool(cand_excused[b, idx].any() or budget_tie[ocand].any())
+        rep.checked["commit"] += idx.size
+        if gfb.any() or ofb.any():
+            # fallback on either side: compare the chosen position
+            win = idx[:P.window]
+            cw = np.nan_to_num(o["confidence"][b, win], nan=-np.inf)
+            top2 = np.sort(cw)[-2:] if cw.size >= 2 else cw
+            near = cw.size >= 2 and (top2[-1] - top2[0]) <= 2 * CONF_TOL
+            if not np.array_equal(gcm, ocm) or not np.array_equal(gfb, ofb):
+                if near or excusable_seq:
+                    rep.excused["fallback_tie"] += 1
+                else:
+                    rep.bad(f"fallback b={b}: gpu {idx[gcm]} oracle {idx[ocm]}")
+            continue
+        for q in np.nonzero(gcm != ocm)[0]:
+            i = idx[q]
+            if cand_excused[b, i]:
+                rep.excused["commit_cascade"] += 1
+            elif ocand[q] and budget_tie[q]:
+                rep.excused["budget_tie"] += 1
+            else:
+                rep.bad(f"commit b={b} i={i}: gpu {gcm[q]} oracle {ocm[q]} N={N[q]:.6g} beta={P.beta}")
+        if np.array_equal(gcm, ocm):
+            if g["n_commit"][b] != ocm.sum():
+                rep.bad(f"n_commit b={b}: gpu {g['n_commit'][b]} oracle {ocm.sum()}")
+            dE = np.abs(g["upstream_entropy"][b, idx] - o["upstream_entropy"][b, idx])
+            tolE = 1e-4 + np.concatenate([[0.0], np.cumsum(dH)[:-1]]) + 1e-6 * np.abs(o["upstream_entropy"][b, idx])
+            fin = np.isfinite(o["upstream_entropy"][b, idx])
+            if np.any((dE > tolE) & fin):
+                q = int(np.argmax((dE > tolE) & fin))
+                rep.bad(f"upstream_entropy b={b} i={idx[q]}: gpu {g['upstream_entropy'][b, idx[q]]:.6g} "
+                        f"oracle {o['upstream_entropy'][b, idx[q]]:.6g}")
+    return rep

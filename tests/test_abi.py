@@ -1,0 +1,119 @@
+"""The C-ABI library loads on the host and exports every symbol that
+include/*.h declares; host-side validation answers without touching a GPU."""
+import ctypes
+import glob
+import math
+import os
+import re
+
+import pytest
+
+from paper_2609_36452_amd import binding as rpd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        txt = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(rpd_[a-z_]+)\s*\(", txt))
+    return names
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert {"rpd_score_commit", "rpd_score_commit_timed", "rpd_gate_commit", "rpd_workspace_size",
+            "rpd_status_string", "rpd_last_error", "rpd_abi_version"} <= names
+    L = ctypes.CDLL(rpd._LIB_PATH)
+    for n in sorted(names):
+        assert hasattr(L, n), n
+
+
+def test_version_and_status_strings():
+    assert rpd.abi_version() == 1
+    assert rpd.status_string(0) == "ok"
+    assert rpd.status_string(4) == "workspace too small"
+
+
+def test_workspace_size():
+    # late-decode LLaDA shape: header + row list + (32 rows x 256 tiles x 16 B)
+    n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=8)
+    assert n == 256 + 1024 + 32 * 256 * 16
+    # 100% masked: 1024 rows x 494 tiles
+    n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=256)
+    assert n == 256 + 1024 + 1024 * 494 * 16
+    assert rpd.workspace_size(0, 1, 256, 4096, 126464, rpd.DTYPE_BF16) == 0
+    assert rpd.workspace_size(65, 1, 256, 4096, 126464, rpd.DTYPE_BF16) == 0
+    assert rpd.workspace_size(4, 1, 256, 4096, 126464, 7) == 0
+
+
+def _call(prob, params, outs, ws=256, ws_bytes=1 << 40):
+    L = rpd.lib()
+    s = L.rpd_score_commit(ctypes.byref(prob) if prob is not None else None,
+                           ctypes.byref(params) if params is not None else None,
+                           ctypes.byref(outs) if outs is not None else None, ws, ws_bytes, None)
+    return s, rpd.last_error()
+
+
+def _fake_outputs():
+    # non-NULL, never dereferenced: validation fails before anything is enqueued
+    return rpd.RpdOutputs(*([4096] * 10 + [None] * 4))
+
+
+def _prob(**kw):
+    base = dict(K=4, B=1, L=256, d=4096, V=126464, dtype=0, hidden=4096, w_u=8192, mask=64, max_masked=8)
+    base.update(kw)
+    return rpd.RpdProblem(base["K"], base["B"], base["L"], base["d"], base["V"], base["dtype"],
+                          base["hidden"], base["w_u"], base["mask"], base["max_masked"])
+
+
+def _params(**kw):
+    p = dict(theta_h=0.9, theta_c=0.6, theta_s=3.5, w=15.0, k_max=6, beta=4.0, window=32, flags=0)
+    p.update(kw)
+    return rpd.RpdParams(**p)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(K=0), 2), (dict(K=65), 2), (dict(B=0), 2), (dict(L=0), 2), (dict(d=0), 2), (dict(V=0), 2),
+    (dict(B=1 << 13, L=1 << 12), 2), (dict(dtype=3), 5), (dict(d=4100), 5), (dict(w_u=8200), 5),
+    (dict(hidden=None), 1), (dict(mask=None), 1),
+])
+def test_problem_validation(kw, status):
+    s, msg = _call(_prob(**kw), _params(), _fake_outputs())
+    assert s == status, msg
+    assert msg
+
+
+@pytest.mark.parametrize("kw", [dict(theta_c=0.95), dict(theta_c=-0.1), dict(w=-1.0), dict(k_max=0),
+                                dict(beta=-1.0), dict(beta=math.nan), dict(window=0), dict(flags=1),
+                                dict(theta_h=math.nan), dict(theta_s=math.inf)])
+def test_param_validation(kw):
+    s, msg = _call(_prob(), _params(**kw), _fake_outputs())
+    assert s == 3, msg
+
+
+def test_null_and_workspace_checks():
+    assert _call(None, _params(), _fake_outputs())[0] == 1
+    assert _call(_prob(), None, _fake_outputs())[0] == 1
+    assert _call(_prob(), _params(), None)[0] == 1
+    o = _fake_outputs()
+    o.drop = None
+    assert _call(_prob(), _params(), o)[0] == 1
+    o = _fake_outputs()
+    o.layer_conf = 4096                       # only one of the three per-layer outputs
+    assert _call(_prob(), _params(), o)[0] == 1
+    s, msg = _call(_prob(), _params(), _fake_outputs(), ws_bytes=1000)
+    assert s == 4 and "needed" in msg
+    assert _call(_prob(), _params(), _fake_outputs(), ws=None)[0] == 1
+    assert _call(_prob(), _params(), _fake_outputs(), ws=256 + 16)[0] == 5
+
+
+def test_gate_validation():
+    L = rpd.lib()
+    q = _params()
+    o = _fake_outputs()
+    assert L.rpd_gate_commit(4, 1, 16, None, 64, 64, 64, ctypes.byref(q), ctypes.byref(o), None) == 1
+    assert L.rpd_gate_commit(0, 1, 16, 64, 64, 64, 64, ctypes.byref(q), ctypes.byref(o), None) == 2
+    bad = _params(beta=-2.0)
+    assert L.rpd_gate_commit(4, 1, 16, 64, 64, 64, 64, ctypes.byref(bad), ctypes.byref(o), None) == 3

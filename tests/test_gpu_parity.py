@@ -1,0 +1,281 @@
+"""Parity of the HIP commit step with the fp64 oracle, through the C ABI.
+
+Small and mid-size cases are compared element by element (every masked
+position, every layer); they span several vocabulary and row tiles, ragged
+vocabulary sizes and hidden sizes that are not multiples of the 64-wide
+k-chunk, and every projection variant (<= 32, <= 64 and > 64 projected rows,
+with row tiles split across XCDs). Full-size LLaDA-8B / Dream-7B shapes are
+compared on sampled positions that the oracle computes one by one, plus the
+prefix-sum identity of the commitment on the GPU's own outputs."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2609_36452_amd import binding as rpd
+from paper_2609_36452_amd.workload import CONFIGS, draw_unembedding, make_workload
+from tests.gpu_util import gpu_params, note, run_gpu, run_oracle, to_device
+from tests.parity import compare, gap_tol, ENTROPY_TOL, CONF_TOL
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _check(w, P, layer=True, **kw):
+    g = run_gpu(w, P, layer_stats=layer, **kw)
+    o = run_oracle(w, P)
+    rep = compare(g, o, w.mask, P, w.cfg.d, layer=layer)
+    note("  " + rep.summary()[:300])
+    assert rep.ok(), rep.summary()
+    masked = int(w.mask.sum())
+    assert sum(rep.excused.values()) <= max(2, 0.05 * masked * (w.cfg.K + 3)), rep.summary()
+    return g, o, rep
+
+
+# -------------------------------------------------------------- tiny fp32 --
+
+@pytest.mark.parametrize("seed", range(12))
+def test_tiny_f32_strict(seed):
+    w = make_workload("tiny", seed)
+    _check(w, O.strict(3, 1.0))
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("pname", ["llada", "dream"])
+def test_tiny_f32_calibrated(seed, pname):
+    cfg = CONFIGS["tiny"].with_(sharp=("calibrated",), unstable_frac=0.3)
+    w = make_workload(cfg, 100 + seed)
+    _check(w, O.LLADA if pname == "llada" else O.DREAM)
+
+
+# ------------------------------------------------- bf16, several variants --
+
+BF16_CASES = [
+    # name, overrides, seed; rows = K * masked
+    ("r32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
+    ("r64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10, masked_frac=None), 12),
+    ("r128_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
+    ("r128_row_split", dict(B=4, L=300, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
+]
+
+
+@pytest.mark.parametrize("name,ov,seed", BF16_CASES, ids=[c[0] for c in BF16_CASES])
+@pytest.mark.parametrize("sharp", ["scaled", "calibrated"])
+def test_bf16_variants(name, ov, seed, sharp):
+    base = CONFIGS["llada_late"].with_(name=name, **ov)
+    if sharp == "calibrated":
+        base = base.with_(sharp=("calibrated",), unstable_frac=0.3)
+    w = make_workload(base, seed)
+    for P in (O.strict(base.K, 1.0), O.LLADA, O.DREAM):
+        _check(w, P)
+
+
+# ------------------------------------------------------------- edge cases --
+
+def _small_bf16(seed=5, **ov):
+    cfg = CONFIGS["llada_late"].with_(name="edge", B=2, L=48, K=4, d=128, V=2000, n_masked=20,
+                                      sharp=("calibrated",), unstable_frac=0.3, **ov)
+    return make_workload(cfg, seed)
+
+
+def test_no_masked_positions():
+    w = _small_bf16(n_masked=0)
+    g = run_gpu(w, O.LLADA, max_masked=0)
+    assert (g["commit"] == 0).all() and (g["token"] == -1).all() and (g["n_commit"] == 0).all()
+    g = run_gpu(w, O.LLADA, max_masked=-1)
+    assert (g["commit"] == 0).all() and (g["n_commit"] == 0).all()
+
+
+def test_all_masked_and_single_layer():
+    w = _small_bf16(n_masked=48)
+    _check(w, O.LLADA)
+    w1 = _small_bf16(n_masked=30, K=1)
+    _check(w1, O.Params(theta_s=1.0, w=1.0))
+
+
+@pytest.mark.parametrize("beta", [0.0, 0.5, 2.0, math.inf])
+def test_budget_extremes(beta):
+    w = _small_bf16(seed=7)
+    P = O.Params(theta_s=2.5, w=20.0, beta=beta)
+    _check(w, P)
+
+
+def test_fewer_masked_than_window_and_tiny_window():
+    w = _small_bf16(seed=8, n_masked=5)
+    _check(w, O.Params(beta=0.0, theta_h=0.999999, theta_c=0.999998))
+    _check(w, O.Params(beta=0.0, window=2, theta_h=0.999999, theta_c=0.999998))
+
+
+def test_nan_in_masked_row_is_contained():
+    w = _small_bf16(seed=9)
+    i = int(np.nonzero(w.mask[0])[0][3])
+    w.hidden[:, 0, i, 5] = np.uint16(0x7FC0)      # one NaN element in every layer's row
+    g = run_gpu(w, O.Params(beta=100.0))
+    assert np.isnan(g["entropy"][0, i]) and np.isnan(g["confidence"][0, i])
+    assert not (g["flags"][0, i] & rpd.FLAG_CANDIDATE)
+    later = np.nonzero(w.mask[0])[0]
+    later = later[later > i]
+    assert not ((g["commit"][0, later] != 0) & ((g["flags"][0, later] & rpd.FLAG_FALLBACK) == 0)).any()
+    _check(w, O.Params(beta=100.0))
+
+
+def test_masked_hint_variants_agree_and_overflow_flagged():
+    w = _small_bf16(seed=10)
+    P = O.DREAM
+    a = run_gpu(w, P)
+    b = run_gpu(w, P, max_masked=-1)
+    c = run_gpu(w, P, max_masked=w.cfg.B * w.cfg.L)
+    for k in a:
+        if k != "status":
+            np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+            np.testing.assert_array_equal(a[k], c[k], err_msg=k)
+    assert a["status"][0] == 0
+    d = run_gpu(w, P, max_masked=w.n_masked - 3)
+    assert d["status"][0] & rpd.DEVICE_STATUS_MASKED_OVERFLOW
+
+
+def test_deterministic_bitwise():
+    w = make_workload(CONFIGS["llada_late"].with_(name="det", d=512, V=9000, L=128, n_masked=40,
+                                                  sharp=("calibrated",)), 21)
+    t = to_device(w)
+    a = run_gpu(w, O.LLADA, tensors=t)
+    b = run_gpu(w, O.LLADA, tensors=t)
+    for k in a:
+        np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+
+
+def test_gate_commit_matches_oracle_selection():
+    rng = np.random.default_rng(3)
+    K, B, L = 6, 3, 200
+    mask = (rng.random((B, L)) < 0.7).astype(np.uint8)
+    y = rng.integers(0, 50, size=(K, B, L)).astype(np.int32)
+    keep = rng.random((B, L)) < 0.7               # many agreeing suffixes
+    for l in range(K - 1):
+        y[l][keep] = y[K - 1][keep]
+    conf = rng.uniform(0.3, 1.0, size=(K, B, L)).astype(np.float32)
+    ent = rng.exponential(0.7, size=(K, B, L)).astype(np.float32)
+    P = O.Params(theta_s=4.5, w=10.0, beta=3.0)
+    pos = O.masked_positions(mask)
+    layer = {"argmax": np.array([y[:, b, i] for b, i in pos]).reshape(-1, K),
+             "conf": np.array([conf[:, b, i] for b, i in pos], np.float64).reshape(-1, K),
+             "entropy": np.array([ent[:, b, i] for b, i in pos], np.float64).reshape(-1, K)}
+    # inside the agreement suffix the final token's probability is the layer's top probability
+    layer["p_final"] = np.where(layer["argmax"] == layer["argmax"][:, -1:], layer["conf"], 0.0)
+    o = O.select(mask, layer, P, pos)
+    dev = "cuda:0"
+    note("  gpu call: gate_commit K=6 B=3 L=200")
+    g = rpd.gate_commit(torch.from_numpy(mask).to(dev), torch.from_numpy(y).to(dev),
+                        torch.from_numpy(conf).to(dev), torch.from_numpy(ent).to(dev), gpu_params(P))
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in g.items()}
+    m = mask != 0
+    np.testing.assert_array_equal(g["token"][m], o["token"][m])
+    np.testing.assert_array_equal(g["persistence"][m], o["persistence"][m])
+    np.testing.assert_allclose(g["drop"][m], o["drop"][m], atol=1e-6)
+    np.testing.assert_allclose(g["stability"][m], o["stability"][m], atol=1e-4)
+    near = np.abs(o["stability"] - P.theta_s) < 1e-4
+    np.testing.assert_array_equal(g["flags"][m & ~near] & 7, o["flags"][m & ~near] & 7)
+    seq_ok = ~near.any(1)
+    for b in np.nonzero(seq_ok)[0]:
+        Nb = o["budget_prefix"][b][m[b]]
+        if np.any(np.abs(Nb - P.beta) < 1e-4):
+            continue
+        np.testing.assert_array_equal(g["commit"][b], o["commit"][b])
+        np.testing.assert_array_equal(g["flags"][b], o["flags"][b])
+        np.testing.assert_allclose(g["upstream_entropy"][b][m[b]], o["upstream_entropy"][b][m[b]], atol=1e-4)
+        assert g["n_commit"][b] == o["n_commit"][b]
+    assert (g["token"][~m] == -1).all() and (g["commit"][~m] == 0).all()
+
+
+# -------------------------------------------------------------- full size --
+
+@pytest.fixture(scope="module")
+def llada_wu():
+    return draw_unembedding(126464, 4096, "bf16", 1)
+
+
+def test_llada_late_full_oracle(llada_wu):
+    """Late-decode LLaDA-8B shape (8 masked of 256, K=4): every position
+    against the full oracle, with the launch configuration the benchmark times."""
+    w = make_workload("llada_late", 1, w_u=llada_wu)
+    for P in (O.strict(4, 1.0), O.LLADA):
+        _check(w, P)
+
+
+def _sampled(w, P, g, nsample, rng):
+    """Oracle per-layer statistics at sampled masked positions, compared with
+    the GPU's; scoring re-derived for those positions from the oracle."""
+    pos = O.masked_positions(w.mask)
+    pick = sorted(rng.choice(len(pos), size=min(nsample, len(pos)), replace=False))
+    sel = [pos[a] for a in pick]
+    st = O.project_layer_stats(w.hidden, w.w_u, w.cfg.dtype, sel)
+    K = w.cfg.K
+    bad = []
+    for a, (b, i) in enumerate(sel):
+        for l in range(K):
+            tie = st["gap"][a, l] < gap_tol(w.cfg.d, st["absbound"][a, l])
+            if abs(g["layer_entropy"][l, b, i] - st["entropy"][a, l]) > ENTROPY_TOL:
+                bad.append(("entropy", l, b, i))
+            if abs(g["layer_conf"][l, b, i] - st["conf"][a, l]) > CONF_TOL:
+                bad.append(("conf", l, b, i))
+            if g["layer_argmax"][l, b, i] != st["argmax"][a, l] and not tie:
+                bad.append(("argmax", l, b, i))
+        k_i = O.persistence(st["argmax"][a])
+        r_i = O.confidence_drop(st["p_final"][a], k_i)
+        if g["persistence"][b, i] != k_i and not (st["gap"][a] < gap_tol(w.cfg.d, st["absbound"][a])).any():
+            bad.append(("persistence", b, i))
+        if g["persistence"][b, i] == k_i and abs(g["drop"][b, i] - r_i) > 2 * CONF_TOL:
+            bad.append(("drop", b, i))
+    assert not bad, bad[:10]
+
+
+def _commit_property(g, mask, P):
+    """Prefix-sum identity on the GPU's own outputs: a candidate is committed
+    iff the entropy of earlier masked non-candidates is within the budget
+    (fp64 recomputation; fp32 near-ties tolerated), else the fallback fired."""
+    B = mask.shape[0]
+    for b in range(B):
+        idx = np.nonzero(mask[b])[0]
+        if idx.size == 0:
+            continue
+        cand = (g["flags"][b, idx] & rpd.FLAG_CANDIDATE) > 0
+        H = g["entropy"][b, idx].astype(np.float64)
+        N = np.concatenate([[0.0], np.cumsum(np.where(cand, 0.0, H))[:-1]])
+        expect = cand & (N <= P.beta)
+        got = g["commit"][b, idx] != 0
+        fb = (g["flags"][b, idx] & rpd.FLAG_FALLBACK) > 0
+        if fb.any():
+            assert not expect[np.abs(N - P.beta) > 1e-3].any()
+            assert got.sum() == 1 and fb.sum() == 1
+            win = idx[:P.window]
+            assert idx[fb][0] in win
+            assert g["confidence"][b, idx[fb][0]] == np.nanmax(g["confidence"][b, win])
+        else:
+            diff = got != expect
+            assert not (diff & (np.abs(N - P.beta) > 1e-3 * (1 + P.beta))).any()
+        assert g["n_commit"][b] == got.sum()
+
+
+@pytest.mark.parametrize("cfgname,seed,nsample", [("llada_100", 2, 12), ("llada_25", 102, 12),
+                                                   ("llada_batched", 4, 10)])
+def test_llada_full_size_sampled(cfgname, seed, nsample, llada_wu):
+    w = make_workload(cfgname, seed, w_u=llada_wu)
+    P = O.strict(4, 1.0)
+    g = run_gpu(w, P)
+    _sampled(w, P, g, nsample, np.random.default_rng(seed))
+    _commit_property(g, w.mask, P)
+
+
+def test_dream_full_size_sampled():
+    w = make_workload("dream_50", 3)
+    for P in (O.strict(4, 1.0), O.DREAM):
+        g = run_gpu(w, P)
+        _commit_property(g, w.mask, P)
+    _sampled(w, P, g, 10, np.random.default_rng(3))
