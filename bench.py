@@ -149,6 +149,10 @@ def main() -> int:
     proj_a = [ev() for _ in range(K)]
     proj_b = [ev() for _ in range(K)]
     start, end = ev(), ev()
+    for e in proj_a + proj_b:       # torch creates the HIP event at its first record
+        e.record()
+    torch.cuda.synchronize()
+    assert all(e.cuda_event for e in proj_a + proj_b)
     log(f"timing {K} steps")
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()

@@ -80,9 +80,9 @@ def test_bf16_variants(name, ov, seed, sharp):
 # ------------------------------------------------------------- edge cases --
 
 def _small_bf16(seed=5, **ov):
-    cfg = CONFIGS["llada_late"].with_(name="edge", B=2, L=48, K=4, d=128, V=2000, n_masked=20,
-                                      sharp=("calibrated",), unstable_frac=0.3, **ov)
-    return make_workload(cfg, seed)
+    kw = dict(name="edge", B=2, L=48, K=4, d=128, V=2000, n_masked=20, sharp=("calibrated",), unstable_frac=0.3)
+    kw.update(ov)
+    return make_workload(CONFIGS["llada_late"].with_(**kw), seed)
 
 
 def test_no_masked_positions():
