@@ -31,6 +31,8 @@ namespace {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr unsigned kFlagCandidate = 1u, kFlagHigh = 2u, kFlagStable = 4u, kFlagCommitted = 8u,
                    kFlagFallback = 16u;
@@ -184,10 +186,10 @@ __device__ __forceinline__ bool map_job(int bid, int nvt, int nrt, int split_row
   return true;
 }
 
-// hidden-state chunk c (TR rows x KC elements) -> registers, zero beyond d or
-// for padding rows (offset -1)
-template <int TR, int KC, int NT, int XPT>
-__device__ __forceinline__ void load_x_chunk(uint4 (&xr)[XPT], const uint16_t* __restrict__ hidden,
+// hidden-state chunk c (TR rows x KC elements) -> registers. GUARD: the
+// chunk may cross d (zero fill past it); otherwise every load is in bounds.
+template <int TR, int KC, int NT, int XPT, bool GUARD>
+__device__ __forceinline__ void load_x_chunk(u32x4 (&xr)[XPT], const uint16_t* __restrict__ hidden,
                                              const long long* xoff, int c, int tid, int d) {
   constexpr int XP = TR * (KC / 8);
 #pragma unroll
@@ -196,35 +198,76 @@ __device__ __forceinline__ void load_x_chunk(uint4 (&xr)[XPT], const uint16_t* _
     if (XP % NT == 0 || q < XP) {
       const int row = q / (KC / 8), c8 = q - row * (KC / 8);
       const int k = c * KC + c8 * 8;
-      const long long off = xoff[row];
-      xr[j] = (off >= 0 && k < d) ? *reinterpret_cast<const uint4*>(hidden + off + k) : make_uint4(0u, 0u, 0u, 0u);
+      const u32x4* src = reinterpret_cast<const u32x4*>(hidden + xoff[row] + k);
+      if (GUARD)
+        xr[j] = k < d ? *src : u32x4{0u, 0u, 0u, 0u};
+      else
+        xr[j] = *src;
     }
   }
 }
 
 template <int TR, int KC, int KCP, int NT, int XPT>
-__device__ __forceinline__ void store_x_chunk(uint16_t (*xsb)[KCP], const uint4 (&xr)[XPT], int tid) {
+__device__ __forceinline__ void store_x_chunk(uint16_t (*xsb)[KCP], const u32x4 (&xr)[XPT], int tid) {
   constexpr int XP = TR * (KC / 8);
 #pragma unroll
   for (int j = 0; j < XPT; ++j) {
     const int q = tid + j * NT;
     if (XP % NT == 0 || q < XP) {
       const int row = q / (KC / 8), c8 = q - row * (KC / 8);
-      *reinterpret_cast<uint4*>(&xsb[row][c8 * 8]) = xr[j];
+      *reinterpret_cast<u32x4*>(&xsb[row][c8 * 8]) = xr[j];
     }
   }
 }
 
-// this lane's W_U operand for chunk c: KS k-steps x MV 16-row blocks
-template <int MV, int KS>
-__device__ __forceinline__ void load_a_chunk(uint4 (&dst)[KS][MV], const uint16_t* __restrict__ w_u,
+// this lane's W_U operand for chunk c: KS 32-wide k-steps x MV 16-row blocks
+template <int MV, int KS, bool GUARD, bool NTA>
+__device__ __forceinline__ void load_a_chunk(u32x4 (&dst)[KS][MV], const uint16_t* __restrict__ w_u,
                                              const long long (&aoff)[MV], int c, int kl, int d) {
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
-    const int k = c * 64 + s * 32;
+    const int k = (c * KS + s) * 32;
 #pragma unroll
-    for (int mv = 0; mv < MV; ++mv)
-      dst[s][mv] = (k + kl < d) ? *reinterpret_cast<const uint4*>(w_u + aoff[mv] + k) : make_uint4(0u, 0u, 0u, 0u);
+    for (int mv = 0; mv < MV; ++mv) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(w_u + aoff[mv] + k);
+      if (GUARD)
+        dst[s][mv] = k + kl < d ? *src : u32x4{0u, 0u, 0u, 0u};
+      else if (NTA)
+        dst[s][mv] = __builtin_nontemporal_load(src);
+      else
+        dst[s][mv] = *src;
+    }
+  }
+}
+
+// MFMAs of one staged chunk. The B fragments (hidden rows, from LDS) of
+// k-step s+1 are read while the MFMAs of step s run, so the LDS latency is
+// hidden even with one wave per SIMD.
+template <int MV, int NB, int KS, int KCP>
+__device__ __forceinline__ void mfma_chunk(f32x4 (&acc)[MV][NB], const u32x4 (&a)[KS][MV],
+                                           const uint16_t (*xsb)[KCP], int lane, int kl) {
+  u32x4 bq[2][NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+    bq[0][nb] = *reinterpret_cast<const u32x4*>(&xsb[nb * 16 + (lane & 15)][kl]);
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    if (s + 1 < KS) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        bq[(s + 1) & 1][nb] = *reinterpret_cast<const u32x4*>(&xsb[nb * 16 + (lane & 15)][(s + 1) * 32 + kl]);
+    }
+    // keep the prefetch of step s+1 ahead of the MFMAs of step s
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const bf16x8 bv = __builtin_bit_cast(bf16x8, bq[s & 1][nb]);
+#pragma unroll
+      for (int mv = 0; mv < MV; ++mv)
+        acc[mv][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[s][mv]), bv, acc[mv][nb],
+                                                               0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -239,20 +282,21 @@ __device__ __forceinline__ void load_a_chunk(uint4 (&dst)[KS][MV], const uint16_
 // The epilogue turns each lane's logits into a softmax state, merges the four
 // lanes of a row and then the waves, and writes one 16-byte partial state per
 // (row, vocab tile).
-template <int NW, int MV, int NB>
+template <int NW, int MV, int NB, int KC, int NSTG, bool NTA>
 __global__ __launch_bounds__(NW * 64) void k_proj_bf16(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
     int nvt, int nrt, int split_rows) {
   constexpr int TR = 16 * NB;
-  constexpr int KC = 64;           // k elements per chunk
+  static_assert(KC % 32 == 0, "a chunk is a whole number of MFMA k-steps");
   constexpr int KS = KC / 32;      // MFMA k-steps per chunk
   constexpr int KCP = KC + 8;      // padded LDS row length (elements)
   constexpr int NT = NW * 64;
   constexpr int XP = TR * (KC / 8);           // 16-byte pieces per hidden chunk
   constexpr int XPT = (XP + NT - 1) / NT;     // pieces per thread
 
-  __shared__ __attribute__((aligned(16))) uint16_t xs[2][TR][KCP];
+  static_assert(NSTG >= 2, "at least double buffering");
+  __shared__ __attribute__((aligned(16))) uint16_t xs[NSTG][TR][KCP];
   __shared__ long long xoff[TR];
   __shared__ float4 red[NW][TR];
 
@@ -267,15 +311,11 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16(
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
 
   for (int t = tid; t < TR; t += NT) {
-    const int r = r0 + t;
-    long long off = -1;
-    if (r < R) {
-      const int p = r / K, l = r - p * K;
-      const int pos = rows[p];
-      const int b = pos / L, i = pos - b * L;
-      off = (((long long)l * B + b) * L + i) * (long long)d;
-    }
-    xoff[t] = off;
+    const int r = r0 + t < R ? r0 + t : r0;   // padding rows re-read a real row; discarded at the end
+    const int p = r / K, l = r - p * K;
+    const int pos = rows[p];
+    const int b = pos / L, i = pos - b * L;
+    xoff[t] = (((long long)l * B + b) * L + i) * (long long)d;
   }
   __syncthreads();
 
@@ -291,42 +331,55 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16(
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[mv][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  uint4 a_cur[KS][MV], a_nxt[KS][MV];
-  uint4 xr[XPT];
-  const int nch = (d + KC - 1) / KC;
+  // NSTG-stage ring: while chunk c is multiplied, the W_U and hidden loads
+  // of chunks c+1 .. c+NSTG-1 are in flight. Buffer indices are compile-time
+  // (the loop is unrolled by NSTG) and the body has no branches, so the
+  // compiler's waits cover exactly the chunk being consumed.
+  u32x4 A[NSTG][KS][MV];
+  u32x4 xr[NSTG][XPT];
+  const int nchf = d / KC;   // full chunks
 
-  load_x_chunk<TR, KC, NT, XPT>(xr, hidden, xoff, 0, tid, d);
-  load_a_chunk<MV, KS>(a_cur, w_u, aoff, 0, kl, d);
-  store_x_chunk<TR, KC, KCP, NT, XPT>(xs[0], xr, tid);
-  __syncthreads();
+#define RPD_LOAD_CHUNK(buf, chunk)                                                  \
+  do {                                                                              \
+    load_x_chunk<TR, KC, NT, XPT, false>(xr[buf], hidden, xoff, (chunk), tid, d);   \
+    load_a_chunk<MV, KS, false, NTA>(A[buf], w_u, aoff, (chunk), kl, d);            \
+  } while (0)
 
-  for (int c = 0; c < nch; ++c) {
-    const int buf = c & 1;
-    const bool more = (c + 1) < nch;
-    if (more) {
-      load_x_chunk<TR, KC, NT, XPT>(xr, hidden, xoff, c + 1, tid, d);
-      load_a_chunk<MV, KS>(a_nxt, w_u, aoff, c + 1, kl, d);
-    }
+  if (nchf > 0) {
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
+    for (int j = 0; j < NSTG - 1; ++j) RPD_LOAD_CHUNK(j, min(j, nchf - 1));
+    store_x_chunk<TR, KC, KCP, NT, XPT>(xs[0], xr[0], tid);
+    __syncthreads();
+    const int nmain = (nchf / NSTG) * NSTG;
+    for (int c0 = 0; c0 < nmain; c0 += NSTG) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const uint4 bq = *reinterpret_cast<const uint4*>(&xs[buf][nb * 16 + (lane & 15)][s * 32 + kl]);
-        const bf16x8 bv = __builtin_bit_cast(bf16x8, bq);
-#pragma unroll
-        for (int mv = 0; mv < MV; ++mv)
-          acc[mv][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a_cur[s][mv]), bv,
-                                                                 acc[mv][nb], 0, 0, 0);
+      for (int j = 0; j < NSTG; ++j) {
+        // chunks past the end re-load the last chunk (never multiplied)
+        RPD_LOAD_CHUNK((j + NSTG - 1) % NSTG, min(c0 + j + NSTG - 1, nchf - 1));
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_chunk<MV, NB, KS, KCP>(acc, A[j], xs[j], lane, kl);
+        store_x_chunk<TR, KC, KCP, NT, XPT>(xs[(j + 1) % NSTG], xr[(j + 1) % NSTG], tid);
+        __syncthreads();
       }
     }
-    if (more) store_x_chunk<TR, KC, KCP, NT, XPT>(xs[buf ^ 1], xr, tid);
-    __syncthreads();
-    if (more) {
+    // fewer than NSTG chunks remain; the ring already holds them in order
+    const int rem = nchf - nmain;
 #pragma unroll
-      for (int s = 0; s < KS; ++s)
-#pragma unroll
-        for (int mv = 0; mv < MV; ++mv) a_cur[s][mv] = a_nxt[s][mv];
+    for (int j = 0; j < NSTG - 1; ++j) {
+      if (j < rem) {
+        mfma_chunk<MV, NB, KS, KCP>(acc, A[j], xs[j], lane, kl);
+        if (j + 1 < rem) store_x_chunk<TR, KC, KCP, NT, XPT>(xs[j + 1], xr[j + 1], tid);
+        __syncthreads();
+      }
     }
+  }
+#undef RPD_LOAD_CHUNK
+  if (d % KC != 0) {   // partial last chunk, zero-filled past d
+    load_x_chunk<TR, KC, NT, XPT, true>(xr[0], hidden, xoff, nchf, tid, d);
+    load_a_chunk<MV, KS, true, false>(A[0], w_u, aoff, nchf, kl, d);
+    store_x_chunk<TR, KC, KCP, NT, XPT>(xs[0], xr[0], tid);
+    __syncthreads();
+    mfma_chunk<MV, NB, KS, KCP>(acc, A[0], xs[0], lane, kl);
   }
 
   // epilogue: softmax state per projected row
@@ -357,6 +410,324 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16(
 #pragma unroll
       for (int w = 1; w < NW; ++w) s = soft_merge(s, soft_unpack(red[w][t]));
       partials[(long long)r * nvt + vt] = soft_pack(s);
+    }
+  }
+}
+
+// ------------------------------------------- K1 projection bf16, 32x32 --
+
+// Large row counts (compute-bound): v_mfma_f32_32x32x16_bf16, which keeps the
+// matrix pipe busy from a single wave per SIMD (the 16x16 form cannot).
+// Workgroup tile: TR = 32*NB projected rows x 32*MV*NW vocabulary rows. As in
+// k_proj_bf16, each wave owns its W_U rows (A operand, straight to
+// registers: lane l holds row l & 31, k elements 8*(l >> 5) .. +8 of each
+// 16-wide k-step) and the hidden rows go through an NSTG-stage LDS ring.
+// Accumulator register q of lane l holds vocabulary row
+// 8*(q >> 2) + 4*(l >> 5) + (q & 3) of its 32-row block and projected row
+// l & 31.
+template <int MV, int KS, bool GUARD>
+__device__ __forceinline__ void load_a_chunk32(u32x4 (&dst)[KS][MV], const uint16_t* __restrict__ w_u,
+                                               const long long (&aoff)[MV], int c, int kl, int d) {
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const int k = (c * KS + s) * 16;
+#pragma unroll
+    for (int mv = 0; mv < MV; ++mv) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(w_u + aoff[mv] + k);
+      if (GUARD)
+        dst[s][mv] = k + kl < d ? *src : u32x4{0u, 0u, 0u, 0u};
+      else
+        dst[s][mv] = *src;
+    }
+  }
+}
+
+template <int MV, int NB, int KS, int KCP>
+__device__ __forceinline__ void mfma_chunk32(f32x16 (&acc)[MV][NB], const u32x4 (&a)[KS][MV],
+                                             const uint16_t (*xsb)[KCP], int lane, int kl) {
+  u32x4 bq[2][NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+    bq[0][nb] = *reinterpret_cast<const u32x4*>(&xsb[nb * 32 + (lane & 31)][kl]);
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    if (s + 1 < KS) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        bq[(s + 1) & 1][nb] = *reinterpret_cast<const u32x4*>(&xsb[nb * 32 + (lane & 31)][(s + 1) * 16 + kl]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const bf16x8 bv = __builtin_bit_cast(bf16x8, bq[s & 1][nb]);
+#pragma unroll
+      for (int mv = 0; mv < MV; ++mv)
+        acc[mv][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[s][mv]), bv, acc[mv][nb],
+                                                               0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <int NW, int MV, int NB, int KC, int NSTG, int MAP = 0>
+__global__ __launch_bounds__(NW * 64) void k_proj_bf16_m32(
+    const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
+    int nvt, int nrt, int split_rows) {
+  constexpr int TR = 32 * NB;
+  static_assert(KC % 16 == 0 && NSTG >= 2, "chunk of whole k-steps, at least double buffering");
+  constexpr int KS = KC / 16;
+  constexpr int KCP = KC + 8;
+  constexpr int NT = NW * 64;
+  constexpr int XP = TR * (KC / 8);
+  constexpr int XPT = (XP + NT - 1) / NT;
+
+  __shared__ __attribute__((aligned(16))) uint16_t xs[NSTG][TR][KCP];
+  __shared__ long long xoff[TR];
+  __shared__ float4 red[NW][TR];
+
+  int rt, vt;
+  if (MAP == 0) {
+    if (!map_job(blockIdx.x, nvt, nrt, split_rows, rt, vt)) return;
+  } else {
+    const int bid = blockIdx.x;
+    if (bid >= nvt * nrt) return;
+    if (MAP == 1) { rt = bid / nvt; vt = bid - rt * nvt; }      // row tiles outer
+    else { vt = bid / nrt; rt = bid - vt * nrt; }               // vocabulary tiles outer
+  }
+  const int R = *n_ptr * K;
+  const int r0 = rt * TR;
+  if (r0 >= R) return;
+  const int vb = (int)((long long)vt * V / nvt);
+  const int ve = (int)((long long)(vt + 1) * V / nvt);
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+
+  for (int t = tid; t < TR; t += NT) {
+    const int r = r0 + t < R ? r0 + t : r0;   // padding rows re-read a real row; discarded at the end
+    const int p = r / K, l = r - p * K;
+    const int pos = rows[p];
+    const int b = pos / L, i = pos - b * L;
+    xoff[t] = (((long long)l * B + b) * L + i) * (long long)d;
+  }
+  __syncthreads();
+
+  const int vw = vb + wid * 32 * MV;
+  const int kl = (lane >> 5) * 8;
+  long long aoff[MV];
+#pragma unroll
+  for (int mv = 0; mv < MV; ++mv) aoff[mv] = (long long)min(vw + mv * 32 + (lane & 31), ve - 1) * d + kl;
+
+  f32x16 acc[MV][NB];
+#pragma unroll
+  for (int mv = 0; mv < MV; ++mv)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[mv][nb][q] = 0.f;
+
+  u32x4 A[NSTG][KS][MV];
+  u32x4 xr[NSTG][XPT];
+  const int nchf = d / KC;
+
+#define RPD_LOAD_CHUNK32(buf, chunk)                                                \
+  do {                                                                              \
+    load_x_chunk<TR, KC, NT, XPT, false>(xr[buf], hidden, xoff, (chunk), tid, d);   \
+    load_a_chunk32<MV, KS, false>(A[buf], w_u, aoff, (chunk), kl, d);               \
+  } while (0)
+
+  if (nchf > 0) {
+#pragma unroll
+    for (int j = 0; j < NSTG - 1; ++j) RPD_LOAD_CHUNK32(j, min(j, nchf - 1));
+    store_x_chunk<TR, KC, KCP, NT, XPT>(xs[0], xr[0], tid);
+    __syncthreads();
+    const int nmain = (nchf / NSTG) * NSTG;
+    for (int c0 = 0; c0 < nmain; c0 += NSTG) {
+#pragma unroll
+      for (int j = 0; j < NSTG; ++j) {
+        RPD_LOAD_CHUNK32((j + NSTG - 1) % NSTG, min(c0 + j + NSTG - 1, nchf - 1));
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_chunk32<MV, NB, KS, KCP>(acc, A[j], xs[j], lane, kl);
+        store_x_chunk<TR, KC, KCP, NT, XPT>(xs[(j + 1) % NSTG], xr[(j + 1) % NSTG], tid);
+        __syncthreads();
+      }
+    }
+    const int rem = nchf - nmain;
+#pragma unroll
+    for (int j = 0; j < NSTG - 1; ++j) {
+      if (j < rem) {
+        mfma_chunk32<MV, NB, KS, KCP>(acc, A[j], xs[j], lane, kl);
+        if (j + 1 < rem) store_x_chunk<TR, KC, KCP, NT, XPT>(xs[j + 1], xr[j + 1], tid);
+        __syncthreads();
+      }
+    }
+  }
+#undef RPD_LOAD_CHUNK32
+  if (d % KC != 0) {
+    load_x_chunk<TR, KC, NT, XPT, true>(xr[0], hidden, xoff, nchf, tid, d);
+    load_a_chunk32<MV, KS, true>(A[0], w_u, aoff, nchf, kl, d);
+    store_x_chunk<TR, KC, KCP, NT, XPT>(xs[0], xr[0], tid);
+    __syncthreads();
+    mfma_chunk32<MV, NB, KS, KCP>(acc, A[0], xs[0], lane, kl);
+  }
+
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    float z[MV * 16];
+    int vi[MV * 16];
+    bool ok[MV * 16];
+#pragma unroll
+    for (int mv = 0; mv < MV; ++mv)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int v = vw + mv * 32 + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
+        z[mv * 16 + q] = acc[mv][nb][q];
+        vi[mv * 16 + q] = v;
+        ok[mv * 16 + q] = v < ve;
+      }
+    Soft st = soft_from_values(z, vi, ok);
+    st = soft_merge(st, soft_shfl_xor(st, 32));
+    if (lane < 32) red[wid][nb * 32 + lane] = soft_pack(st);
+  }
+  __syncthreads();
+  for (int t = tid; t < TR; t += NT) {
+    const int r = r0 + t;
+    if (r < R) {
+      Soft sres = soft_unpack(red[0][t]);
+#pragma unroll
+      for (int w = 1; w < NW; ++w) sres = soft_merge(sres, soft_unpack(red[w][t]));
+      partials[(long long)r * nvt + vt] = soft_pack(sres);
+    }
+  }
+}
+
+// Small row counts (TR = 16*NB >= all projected rows): no LDS staging and no
+// barrier in the main loop. Each wave owns 16*MV consecutive W_U rows of the
+// workgroup's vocabulary range and streams them through a DEPTH-deep register
+// pipeline with non-temporal loads (W_U is read exactly once per call); the
+// hidden rows, at most 16*NB of them, are read by every wave straight from L2
+// in the MFMA B-operand layout. Rows past the last projected row read row 0
+// again and are discarded in the epilogue.
+template <int NW, int MV, int NB, int DEPTH>
+__global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
+    const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V, int nvt) {
+  constexpr int TR = 16 * NB;
+  constexpr int NS = DEPTH + 1;
+  __shared__ float4 red[NW][TR];
+
+  const int R = *n_ptr * K;
+  if (R <= 0) return;
+  // workgroup ids are dispatched round-robin over the XCDs: give each XCD a
+  // contiguous range of vocabulary tiles
+  const int vt = (int)(((long long)(blockIdx.x & 7) * nvt) / 8) + (blockIdx.x >> 3);
+  if (vt >= (int)(((long long)((blockIdx.x & 7) + 1) * nvt) / 8)) return;
+  const int vb = (int)((long long)vt * V / nvt);
+  const int ve = (int)((long long)(vt + 1) * V / nvt);
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int vw = vb + wid * 16 * MV;
+  const int kl = (lane >> 4) * 8;
+
+  long long aoff[MV];
+#pragma unroll
+  for (int mv = 0; mv < MV; ++mv) aoff[mv] = (long long)min(vw + mv * 16 + (lane & 15), ve - 1) * d + kl;
+  long long boff[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    int r = nb * 16 + (lane & 15);
+    r = r < R ? r : 0;
+    const int p = r / K, l = r - p * K;
+    const int pos = rows[p];
+    const int b = pos / L, i = pos - b * L;
+    boff[nb] = (((long long)l * B + b) * L + i) * (long long)d + kl;
+  }
+
+  f32x4 acc[MV][NB];
+#pragma unroll
+  for (int mv = 0; mv < MV; ++mv)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mv][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 A[NS][MV], X[NS][NB];
+  const u32x4 z4 = {0u, 0u, 0u, 0u};
+
+  // full 32-wide k-steps: every lane in bounds, loads are unconditional
+#define RPD_LOAD_STEP(buf, step)                                                                  \
+  do {                                                                                            \
+    const int k_ = (step) * 32;                                                                   \
+    _Pragma("unroll") for (int mv = 0; mv < MV; ++mv) A[buf][mv] =                               \
+        __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(w_u + aoff[mv] + k_));          \
+    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb) X[buf][nb] =                               \
+        *reinterpret_cast<const u32x4*>(hidden + boff[nb] + k_);                                  \
+  } while (0)
+#define RPD_MFMA_STEP(buf)                                                                        \
+  do {                                                                                            \
+    _Pragma("unroll") for (int nb = 0; nb < NB; ++nb)                                            \
+    _Pragma("unroll") for (int mv = 0; mv < MV; ++mv)                                            \
+      acc[mv][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, A[buf][mv]), \
+                                                             __builtin_bit_cast(bf16x8, X[buf][nb]), \
+                                                             acc[mv][nb], 0, 0, 0);               \
+  } while (0)
+
+  const int nkf = d / 32;
+  if (nkf > 0) {
+#pragma unroll
+    for (int j = 0; j < DEPTH; ++j) RPD_LOAD_STEP(j, min(j, nkf - 1));
+    const int nmain = (nkf / NS) * NS;
+    for (int s0 = 0; s0 < nmain; s0 += NS) {
+#pragma unroll
+      for (int j = 0; j < NS; ++j) {
+        // steps past the end re-load the last step (discarded); the
+        // scheduling barrier keeps these loads ahead of this step's MFMAs
+        RPD_LOAD_STEP((j + DEPTH) % NS, min(s0 + j + DEPTH, nkf - 1));
+        __builtin_amdgcn_sched_barrier(0);
+        RPD_MFMA_STEP(j);
+      }
+    }
+    // the remaining (< NS) steps were loaded by the last group into buffers 0..
+    const int rem = nkf - nmain;
+#pragma unroll
+    for (int j = 0; j < NS - 1; ++j)
+      if (j < rem) RPD_MFMA_STEP(j);
+  }
+  if (d % 32 != 0) {   // partial last k-step (d is a multiple of 8)
+    const int k_ = nkf * 32;
+    const bool in_ = k_ + kl < d;
+#pragma unroll
+    for (int mv = 0; mv < MV; ++mv)
+      A[0][mv] = in_ ? *reinterpret_cast<const u32x4*>(w_u + aoff[mv] + k_) : z4;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) X[0][nb] = in_ ? *reinterpret_cast<const u32x4*>(hidden + boff[nb] + k_) : z4;
+    RPD_MFMA_STEP(0);
+  }
+#undef RPD_MFMA_STEP
+#undef RPD_LOAD_STEP
+
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    float z[MV * 4];
+    int vi[MV * 4];
+    bool ok[MV * 4];
+#pragma unroll
+    for (int mv = 0; mv < MV; ++mv)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int v = vw + mv * 16 + (lane >> 4) * 4 + e;
+        z[mv * 4 + e] = acc[mv][nb][e];
+        vi[mv * 4 + e] = v;
+        ok[mv * 4 + e] = v < ve;
+      }
+    Soft st = soft_from_values(z, vi, ok);
+    st = soft_merge(st, soft_shfl_xor(st, 16));
+    st = soft_merge(st, soft_shfl_xor(st, 32));
+    if (lane < 16) red[wid][nb * 16 + lane] = soft_pack(st);
+  }
+  __syncthreads();
+  for (int t = tid; t < TR; t += NW * 64) {
+    if (t < R) {
+      Soft sres = soft_unpack(red[0][t]);
+#pragma unroll
+      for (int w = 1; w < NW; ++w) sres = soft_merge(sres, soft_unpack(red[w][t]));
+      partials[(long long)t * nvt + vt] = soft_pack(sres);
     }
   }
 }
@@ -454,39 +825,52 @@ struct ScoreArgs {
   float* layer_entropy;
 };
 
-// One wave per masked position: merge the vocab-tile states of each of its K
-// rows (lane-strided in tile order, then a fixed butterfly), giving every
-// lane the layer's argmax, top probability and entropy; lane l keeps layer
-// l. Persistence, drop and stability are then evaluated across lanes.
-__global__ __launch_bounds__(256) void k_reduce_score(const float4* __restrict__ partials,
-                                                       const int32_t* __restrict__ rows,
-                                                       const int32_t* __restrict__ n_ptr, int nvt, ScoreArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int p = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+// One workgroup of four waves per masked position. Wave w merges the
+// vocab-tile states of layers w, w+4, ...: each lane folds tiles lane,
+// lane+64, ... in tile order (loads batched four at a time), then a fixed
+// xor butterfly combines the lanes. Wave 0 then evaluates persistence, drop
+// and stability with one lane per layer.
+constexpr int kReduceWaves = 4;
+
+__global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4* __restrict__ partials,
+                                                                     const int32_t* __restrict__ rows,
+                                                                     const int32_t* __restrict__ n_ptr, int nvt,
+                                                                     ScoreArgs a) {
+  __shared__ int ly[64];
+  __shared__ float lc[64], lh[64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int p = blockIdx.x;
   if (p >= *n_ptr) return;
   const int pos = rows[p];
   const int b = pos / a.L, i = pos - b * a.L;
-  int my_y = -1;
-  float my_c = 0.f, my_h = 0.f;
-  for (int l = 0; l < a.K; ++l) {
+  const float4 empty = soft_pack(soft_empty());
+  for (int l = wid; l < a.K; l += kReduceWaves) {
     const float4* src = partials + ((long long)p * a.K + l) * nvt;
     Soft s = soft_empty();
-    for (int t = lane; t < nvt; t += 64) s = soft_merge(s, soft_unpack(src[t]));
+    for (int t0 = lane; t0 < nvt; t0 += 64 * 4) {
+      float4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = (t0 + 64 * u < nvt) ? src[t0 + 64 * u] : empty;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) s = soft_merge(s, soft_unpack(v[u]));
+    }
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) s = soft_merge(s, soft_shfl_xor(s, m));
-    const float c = 1.0f / s.S;
-    const float h = fmaxf(logf(s.S) - s.T / s.S, 0.0f);
-    const float h_out = (s.S != s.S) ? s.S : h;   // keep NaN visible
-    const int y = (s.idx == INT_MAX) ? -1 : s.idx;
-    if (lane == l) {
-      my_y = y;
-      my_c = c;
-      my_h = h_out;
+    if (lane == 0) {
+      const float h = fmaxf(logf(s.S) - s.T / s.S, 0.0f);
+      ly[l] = (s.idx == INT_MAX) ? -1 : s.idx;
+      lc[l] = 1.0f / s.S;
+      lh[l] = (s.S != s.S) ? s.S : h;   // keep NaN visible
     }
   }
-  const int yK = __shfl(my_y, a.K - 1);
-  const float cK = __shfl(my_c, a.K - 1);
-  const float hK = __shfl(my_h, a.K - 1);
+  __syncthreads();
+  if (wid != 0) return;
+  const int my_y = lane < a.K ? ly[lane] : -1;
+  const float my_c = lane < a.K ? lc[lane] : 0.f;
+  const float my_h = lane < a.K ? lh[lane] : 0.f;
+  const int yK = ly[a.K - 1];
+  const float cK = lc[a.K - 1];
+  const float hK = lh[a.K - 1];
   // Eq. 2: agreement suffix ending at the final layer
   const unsigned long long dis = __ballot(lane < a.K && my_y != yK);
   const int last_dis = dis ? 63 - __clzll(dis) : -1;
@@ -740,10 +1124,10 @@ CommitArgs commit_args(const Launch& a) {
   return c;
 }
 
-template <int NW, int MV, int NB>
+template <int NW, int MV, int NB, int KC, int NSTG, bool NTA>
 void launch_proj_bf16(const Launch& a, hipStream_t s) {
   const ProjPlan& p = a.plan;
-  hipLaunchKernelGGL((k_proj_bf16<NW, MV, NB>), dim3(p.grid), dim3(NW * 64), 0, s,
+  hipLaunchKernelGGL((k_proj_bf16<NW, MV, NB, KC, NSTG, NTA>), dim3(p.grid), dim3(NW * 64), 0, s,
                      static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
                      a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows);
 }
@@ -775,9 +1159,9 @@ ProjPlan plan_projection(int dtype, long long rows_cap, int V) {
     nvt = ((nvt + 255) / 256) * 256;
     p.nvt = nvt < V ? nvt : V;
   } else {
-    p.variant = PROJ_BF16_R128;
+    p.variant = PROJ_BF16_M32;
     p.rows_per_tile = 128;
-    p.vocab_cap = 4 * 64;
+    p.vocab_cap = 8 * 64;
     p.nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
   }
   p.nrt = (int)((rows_cap + p.rows_per_tile - 1) / p.rows_per_tile);
@@ -796,9 +1180,13 @@ hipError_t launch_compact(const Launch& a, hipStream_t s) {
 hipError_t launch_projection(const Launch& a, hipStream_t s) {
   if (a.max_masked <= 0) return hipSuccess;
   switch (a.plan.variant) {
-    case PROJ_BF16_R32: launch_proj_bf16<8, 4, 2>(a, s); break;
-    case PROJ_BF16_R64: launch_proj_bf16<8, 4, 4>(a, s); break;
-    case PROJ_BF16_R128: launch_proj_bf16<4, 4, 8>(a, s); break;
+    case PROJ_BF16_R32: launch_proj_bf16<8, 4, 2, 64, 3, false>(a, s); break;
+    case PROJ_BF16_R64: launch_proj_bf16<8, 4, 4, 64, 3, false>(a, s); break;
+    case PROJ_BF16_M32:
+      hipLaunchKernelGGL((k_proj_bf16_m32<8, 2, 4, 64, 2>), dim3(a.plan.grid), dim3(512), 0, s,
+                         static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
+                         a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, a.plan.nvt, a.plan.nrt, a.plan.split_rows);
+      break;
     case PROJ_F32:
       hipLaunchKernelGGL(k_proj_f32, dim3(a.plan.grid), dim3(256), 0, s, static_cast<const float*>(a.hidden),
                          static_cast<const float*>(a.w_u), a.rows, a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V,
@@ -810,14 +1198,18 @@ hipError_t launch_projection(const Launch& a, hipStream_t s) {
 
 hipError_t launch_reduce_score(const Launch& a, hipStream_t s) {
   if (a.max_masked <= 0) return hipSuccess;
-  const int per_wg = 4;
-  hipLaunchKernelGGL(k_reduce_score, dim3((a.max_masked + per_wg - 1) / per_wg), dim3(64 * per_wg), 0, s,
-                     a.partials, a.rows, a.n_masked, a.plan.nvt, score_args(a));
+  hipLaunchKernelGGL(k_reduce_score, dim3(a.max_masked), dim3(64 * kReduceWaves), 0, s, a.partials, a.rows,
+                     a.n_masked, a.plan.nvt, score_args(a));
   return hipGetLastError();
 }
 
+int commit_threads(int L) {
+  const int t = ((L + 63) / 64) * 64;
+  return t < kCommitThreads ? t : kCommitThreads;
+}
+
 hipError_t launch_commit(const Launch& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_commit, dim3(a.B), dim3(kCommitThreads), 0, s, a.mask, commit_args(a));
+  hipLaunchKernelGGL(k_commit, dim3(a.B), dim3(commit_threads(a.L)), 0, s, a.mask, commit_args(a));
   return hipGetLastError();
 }
 
@@ -828,7 +1220,7 @@ hipError_t launch_gate_commit(const Launch& a, const int32_t* l_y, const float* 
                      score_args(a));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_commit, dim3(a.B), dim3(kCommitThreads), 0, s, a.mask, commit_args(a));
+  hipLaunchKernelGGL(k_commit, dim3(a.B), dim3(commit_threads(a.L)), 0, s, a.mask, commit_args(a));
   return hipGetLastError();
 }
 

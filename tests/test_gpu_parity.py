@@ -61,8 +61,9 @@ BF16_CASES = [
     # name, overrides, seed; rows = K * masked
     ("r32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
     ("r64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10, masked_frac=None), 12),
-    ("r128_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
-    ("r128_row_split", dict(B=4, L=300, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
+    ("m32_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
+    ("m32_row_split", dict(B=4, L=300, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
+    ("m32_one_tile", dict(B=1, L=40, K=4, d=4104, V=2500, n_masked=20, masked_frac=None), 15),
 ]
 
 
