@@ -36,13 +36,20 @@ def test_version_and_status_strings():
     assert rpd.status_string(4) == "workspace too small"
 
 
+def _a256(x):
+    return (x + 255) // 256 * 256
+
+
 def test_workspace_size():
     # late-decode LLaDA shape: header + row list + (32 rows x 256 tiles x 16 B)
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=8)
-    assert n == 256 + 1024 + 32 * 256 * 16
-    # 100% masked: 1024 rows x 247 tiles of 512 vocabulary rows
+    assert n == 256 + 1024 + _a256(32 * 256 * 16)
+    # 10% masked: 104 rows x 247 tiles of 512 vocabulary rows
+    n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=26)
+    assert n == 256 + 1024 + _a256(104 * 247 * 16)
+    # 100% masked: 1024 rows x 494 tiles of 256 vocabulary rows
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=256)
-    assert n == 256 + 1024 + 1024 * 247 * 16
+    assert n == 256 + 1024 + _a256(1024 * 494 * 16)
     assert rpd.workspace_size(0, 1, 256, 4096, 126464, rpd.DTYPE_BF16) == 0
     assert rpd.workspace_size(65, 1, 256, 4096, 126464, rpd.DTYPE_BF16) == 0
     assert rpd.workspace_size(4, 1, 256, 4096, 126464, 7) == 0

@@ -3,8 +3,8 @@
 Small and mid-size cases are compared element by element (every masked
 position, every layer); they span several vocabulary and row tiles, ragged
 vocabulary sizes and hidden sizes that are not multiples of the 64-wide
-k-chunk, and every projection variant (<= 32, <= 64 and > 64 projected rows,
-with row tiles split across XCDs). Full-size LLaDA-8B / Dream-7B shapes are
+k-chunk, and every projection variant (<= 32, <= 64, <= 192 and more
+projected rows, with row tiles split across XCDs). Full-size LLaDA-8B / Dream-7B shapes are
 compared on sampled positions that the oracle computes one by one, plus the
 prefix-sum identity of the commitment on the GPU's own outputs."""
 import math
@@ -61,9 +61,10 @@ BF16_CASES = [
     # name, overrides, seed; rows = K * masked
     ("r32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
     ("r64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10, masked_frac=None), 12),
-    ("m32_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
-    ("m32_row_split", dict(B=4, L=300, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
     ("m32_one_tile", dict(B=1, L=40, K=4, d=4104, V=2500, n_masked=20, masked_frac=None), 15),
+    ("m32_two_tiles", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=20, masked_frac=None), 16),
+    ("big_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
+    ("big_row_split", dict(B=4, L=600, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
 ]
 
 
@@ -133,10 +134,16 @@ def test_masked_hint_variants_agree_and_overflow_flagged():
     a = run_gpu(w, P)
     b = run_gpu(w, P, max_masked=-1)
     c = run_gpu(w, P, max_masked=w.cfg.B * w.cfg.L)
+    # the exact count and -1 plan the same tiling: identical bits. A looser
+    # bound may select another projection tiling, which changes only the
+    # order of the fp32 sums: the discrete outputs agree, floats to rounding.
     for k in a:
         if k != "status":
             np.testing.assert_array_equal(a[k], b[k], err_msg=k)
-            np.testing.assert_array_equal(a[k], c[k], err_msg=k)
+            if a[k].dtype.kind == "f":
+                np.testing.assert_allclose(a[k], c[k], rtol=1e-5, atol=1e-5, err_msg=k)
+            else:
+                np.testing.assert_array_equal(a[k], c[k], err_msg=k)
     assert a["status"][0] == 0
     d = run_gpu(w, P, max_masked=w.n_masked - 3)
     assert d["status"][0] & rpd.DEVICE_STATUS_MASKED_OVERFLOW
