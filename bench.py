@@ -27,21 +27,40 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
 RIDGE_ROWS = 315             # projected rows where the projection turns compute-bound
 
 METRIC = "masked positions scored+committed/sec at LLaDA-8B shape; MFMA % / HBM GB/s"
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_36452_amd", "csrc", "rpd_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2609_36452_amd", "csrc")
+# the source files that define each projection variant's kernel
+VARIANT_SOURCES = {
+    "bf16_r32": ["rpd_device.h", "proj_stage.h", "proj_small.hip"],
+    "bf16_r64": ["rpd_device.h", "proj_stage.h", "proj_small.hip"],
+    "bf16_m32": ["rpd_device.h", "proj_stage.h", "proj_mid.hip"],
+    "bf16_big": ["rpd_device.h", "proj_big.hip"],
+    "f32": ["rpd_device.h", "proj_f32.hip"],
+}
+VARIANT_KERNEL = {"bf16_r32": "k_proj_bf16", "bf16_r64": "k_proj_bf16", "bf16_m32": "k_proj_bf16_m32",
+                  "bf16_big": "k_proj_bf16_big", "f32": "k_proj_f32"}
+COPY_PROBE_BYTES = 1 << 30     # fp32 elements read (and as many written) by the copy probe
 
 
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_source_sha() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+def kernel_source_sha(variant: str) -> str:
+    h = hashlib.sha256()
+    for f in VARIANT_SOURCES[variant]:
+        h.update(open(os.path.join(CSRC, f), "rb").read())
+    return h.hexdigest()[:16]
 
 
-def read_traffic(workload: str):
+def traffic_path(variant: str, workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"proj_{variant}_{workload}_traffic.txt")
+
+
+def read_traffic(variant: str, workload: str):
     """HBM bytes per projection launch from the committed rocprofv3 counter
-    summary of this workload, if it was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"k_proj_bf16_{workload}_traffic.txt")
+    summary of this workload, if it was taken on the current source of the
+    kernel; else None."""
+    path = traffic_path(variant, workload)
     if not os.path.exists(path):
         return None
     kv = {}
@@ -49,12 +68,27 @@ def read_traffic(workload: str):
         if "=" in line and not line.lstrip().startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("kernel_source_sha") != kernel_source_sha():
+    if kv.get("kernel_source_sha") != kernel_source_sha(variant):
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def copy_probe(torch) -> None:
+    """A plain streaming copy of known size (read COPY_PROBE_BYTES, write as
+    many) for scaling the HBM byte counters: three launches of torch.neg on
+    fp32 buffers far larger than the last-level cache."""
+    n = COPY_PROBE_BYTES // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    log(f"copy probe: 3 launches, each reads {COPY_PROBE_BYTES} B and writes {COPY_PROBE_BYTES} B")
+    del src, dst
 
 
 def blas_threads() -> int:
@@ -80,7 +114,7 @@ def cpu_baseline(w, P, budget_s: float) -> dict:
     O.assemble(w.mask, pos, layer, P)
     t = time.perf_counter() - t0
     reps = 1
-    while t * (reps + 1) / reps < budget_s and reps < 8:
+    while t * (reps + 1) / reps < budget_s and reps < 256:
         t0 = time.perf_counter()
         pos, layer = O.layer_stats_masked(w.hidden, w.w_u, w.mask, w.cfg.dtype)
         O.assemble(w.mask, pos, layer, P)
@@ -103,6 +137,8 @@ def main() -> int:
     ap.add_argument("--beta", type=float, default=1.0)
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain copy kernel of known size (for scaling HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the commit step is benchmarked on a single MI355X "
@@ -138,6 +174,8 @@ def main() -> int:
         w_u = torch.from_numpy(w.w_u).to(dev)
     mask = torch.from_numpy(w.mask).to(dev)
     call = rpd.ScoreCommit(hidden, w_u, mask, P, max_masked=w.n_masked)
+    variant = rpd.projection_variant(cfg.K, cfg.B, cfg.L, cfg.d, cfg.V, hidden.dtype, max_masked=w.n_masked)
+    log(f"projection variant {variant}")
     torch.cuda.synchronize()
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -182,8 +220,8 @@ def main() -> int:
         achieved = flops_alg / (proj_avg / 1e3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4)}
-    roof["traffic"] = read_traffic(cfg.name)
-    roof["kernel"] = "k_proj_bf16" if cfg.dtype == "bf16" else "k_proj_f32"
+    roof["traffic"] = read_traffic(variant, cfg.name)
+    roof["kernel"] = f"{VARIANT_KERNEL[variant]} ({variant})"
     roof["kernel_us"] = round(proj_avg * 1e3, 2)
     roof["alg_bytes_per_launch"] = bytes_alg
     roof["alg_flops_per_launch"] = flops_alg
@@ -207,6 +245,8 @@ def main() -> int:
         "iterations_per_s": round(1e3 / ms_step, 1),
         "roofline": roof,
     }
+    if args.copy_probe:
+        copy_probe(torch)
     if not args.no_cpu_baseline:
         import oracle as O
         OP = O.Params(**P.__dict__)

@@ -192,6 +192,24 @@ rpd_status rpd_gate_commit(int32_t K, int32_t B, int32_t L, const uint8_t* mask,
                            const float* layer_entropy, const rpd_params* q,
                            const rpd_outputs* o, void* stream);
 
+/* projection kernel variants (values of rpd_projection_variant) */
+enum {
+  RPD_PROJ_BF16_R32 = 0, /* bf16, at most 32 projected rows: HBM-bound W_U stream */
+  RPD_PROJ_BF16_R64 = 1, /* bf16, 33..64 rows */
+  RPD_PROJ_BF16_M32 = 2, /* bf16, 65..192 rows */
+  RPD_PROJ_F32 = 3,      /* fp32 inputs, any row count */
+  RPD_PROJ_BF16_BIG = 4  /* bf16, more than 192 rows: MFMA-bound 256 x 256 tiles */
+};
+
+/*
+ * The projection kernel variant (RPD_PROJ_*) that rpd_score_commit launches
+ * for problem `p` (pointers in `p` are not read), where the projected rows
+ * are K * max_masked; with max_masked < 0 this assumes every position is
+ * masked (the call itself plans for the count it reads back). Returns -1 if
+ * the shape or dtype is invalid. For instrumentation and tests.
+ */
+int32_t rpd_projection_variant(const rpd_problem* p);
+
 /* Static text for a status code. */
 const char* rpd_status_string(rpd_status s);
 

@@ -115,6 +115,8 @@ def lib() -> ctypes.CDLL:
         L.rpd_status_string.argtypes = [ctypes.c_int]
         L.rpd_last_error.restype = ctypes.c_char_p
         L.rpd_last_error.argtypes = []
+        L.rpd_projection_variant.restype = ctypes.c_int32
+        L.rpd_projection_variant.argtypes = [ctypes.POINTER(RpdProblem)]
         L.rpd_abi_version.restype = ctypes.c_int32
         L.rpd_abi_version.argtypes = []
         _lib = L
@@ -159,6 +161,21 @@ def workspace_size(K: int, B: int, L: int, d: int, V: int, dtype: torch.dtype | 
     code = dtype if isinstance(dtype, int) else (DTYPE_BF16 if dtype == torch.bfloat16 else DTYPE_F32)
     p = make_problem(K, B, L, d, V, code, max_masked=max_masked)
     return int(lib().rpd_workspace_size(ctypes.byref(p)))
+
+
+PROJ_VARIANTS = {0: "bf16_r32", 1: "bf16_r64", 2: "bf16_m32", 3: "f32", 4: "bf16_big"}
+
+
+def projection_variant(K: int, B: int, L: int, d: int, V: int, dtype: torch.dtype | int,
+                       max_masked: int = -1) -> str:
+    """Name of the projection kernel variant rpd_score_commit launches for
+    this shape (rpd_projection_variant)."""
+    code = dtype if isinstance(dtype, int) else (DTYPE_BF16 if dtype == torch.bfloat16 else DTYPE_F32)
+    p = make_problem(K, B, L, d, V, code, max_masked=max_masked)
+    v = int(lib().rpd_projection_variant(ctypes.byref(p)))
+    if v < 0:
+        raise RpdError(2, f"invalid shape or dtype for a plan: K={K} B={B} L={L} d={d} V={V} dtype={code}")
+    return PROJ_VARIANTS[v]
 
 
 def alloc_outputs(K: int, B: int, L: int, device, layer_stats: bool = False) -> dict:

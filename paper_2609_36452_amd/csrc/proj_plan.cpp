@@ -1,0 +1,59 @@
+// Host side of the projection: the tile plan for a row bound, and the
+// dispatch to the kernel variant it names.
+#include "rpd_launch.h"
+
+namespace rpd {
+
+ProjPlan plan_projection(int dtype, long long rows_cap, int V) {
+  ProjPlan p{};
+  if (rows_cap < 1) rows_cap = 1;
+  if (dtype == 1) {   // fp32
+    p.variant = PROJ_F32;
+    p.rows_per_tile = 16;
+    p.vocab_cap = 64;
+    p.nvt = (V + 63) / 64;
+    p.nrt = (int)((rows_cap + 15) / 16);
+    p.split_rows = 0;
+    p.per_xcd = 0;
+    p.grid = p.nvt * p.nrt;
+    return p;
+  }
+  if (rows_cap <= 64) {
+    p.variant = rows_cap <= 32 ? PROJ_BF16_R32 : PROJ_BF16_R64;
+    p.rows_per_tile = rows_cap <= 32 ? 32 : 64;
+    p.vocab_cap = 8 * 64;
+    // every CU streams an equal share of W_U: a multiple of 256 tiles
+    int nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
+    nvt = ((nvt + 255) / 256) * 256;
+    p.nvt = nvt < V ? nvt : V;
+  } else if (rows_cap <= 192) {
+    p.variant = PROJ_BF16_M32;
+    p.rows_per_tile = 128;
+    p.vocab_cap = 8 * 64;
+    p.nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
+  } else {
+    p.variant = PROJ_BF16_BIG;
+    p.rows_per_tile = kBigTileRows;
+    p.vocab_cap = kBigTileVocab;
+    p.nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
+  }
+  p.nrt = (int)((rows_cap + p.rows_per_tile - 1) / p.rows_per_tile);
+  p.split_rows = p.nrt >= 8 ? 1 : 0;
+  p.per_xcd = p.split_rows ? ((p.nrt + 7) / 8) * p.nvt : ((p.nvt + 7) / 8) * p.nrt;
+  p.grid = 8 * p.per_xcd;
+  return p;
+}
+
+hipError_t launch_projection(const Launch& a, hipStream_t s) {
+  if (a.max_masked <= 0) return hipSuccess;
+  switch (a.plan.variant) {
+    case PROJ_BF16_R32:
+    case PROJ_BF16_R64: return launch_proj_small(a, s);
+    case PROJ_BF16_M32: return launch_proj_mid(a, s);
+    case PROJ_BF16_BIG: return launch_proj_big(a, s);
+    case PROJ_F32: return launch_proj_f32(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace rpd

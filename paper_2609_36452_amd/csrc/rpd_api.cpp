@@ -1,5 +1,6 @@
 // C ABI of the RPD commit step: argument validation, workspace layout,
-// launch planning and error reporting. Kernels live in rpd_kernels.hip.
+// launch planning and error reporting. Kernels live in proj_*.hip and
+// score_commit.hip; the projection plan in proj_plan.cpp.
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -111,6 +112,11 @@ extern "C" {
 size_t rpd_workspace_size(const rpd_problem* p) {
   if (!p || !shape_ok(p) || (p->dtype != RPD_DTYPE_BF16 && p->dtype != RPD_DTYPE_F32)) return 0;
   return workspace_bytes_for(p, masked_cap(p));
+}
+
+int32_t rpd_projection_variant(const rpd_problem* p) {
+  if (!p || !shape_ok(p) || (p->dtype != RPD_DTYPE_BF16 && p->dtype != RPD_DTYPE_F32)) return -1;
+  return (int32_t)rpd::plan_projection(p->dtype, (long long)p->K * masked_cap(p), p->V).variant;
 }
 
 static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, const rpd_outputs* o,

@@ -1,5 +1,6 @@
-// Internal interface between the C ABI (rpd_api.cpp) and the gfx950 kernels
-// (rpd_kernels.hip). Not installed; no torch or HIP types beyond hipStream_t.
+// Internal interface between the C ABI (rpd_api.cpp), the projection plan
+// (proj_plan.cpp) and the gfx950 kernels (proj_*.hip, score_commit.hip).
+// Not installed; no torch or HIP types beyond hipStream_t.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -17,6 +18,9 @@ enum ProjVariant {
   PROJ_F32 = 3,        // fp32 inputs: vector ALU, 16 rows x 64 vocab
   PROJ_BF16_BIG = 4,   // compute-bound: 256 x 256 tiles, both operands through LDS
 };
+
+// tile of the large-row variant: vocabulary rows x projected rows
+constexpr int kBigTileVocab = 256, kBigTileRows = 256;
 
 struct ProjPlan {
   ProjVariant variant;
@@ -61,6 +65,12 @@ hipError_t launch_compact(const Launch& a, hipStream_t s);
 hipError_t launch_projection(const Launch& a, hipStream_t s);
 hipError_t launch_reduce_score(const Launch& a, hipStream_t s);
 hipError_t launch_commit(const Launch& a, hipStream_t s);
+
+// the projection variants, dispatched by launch_projection on a.plan.variant
+hipError_t launch_proj_small(const Launch& a, hipStream_t s);   // PROJ_BF16_R32, PROJ_BF16_R64
+hipError_t launch_proj_mid(const Launch& a, hipStream_t s);     // PROJ_BF16_M32
+hipError_t launch_proj_big(const Launch& a, hipStream_t s);     // PROJ_BF16_BIG
+hipError_t launch_proj_f32(const Launch& a, hipStream_t s);     // PROJ_F32
 
 // scoring + commitment from caller-supplied per-layer statistics
 hipError_t launch_gate_commit(const Launch& a, const int32_t* layer_argmax, const float* layer_conf,

@@ -1,0 +1,411 @@
+// K0 masked-position compaction, K2 cross-tile reduction with the
+// layerwise stability test (Eq. 2-5), K3 budgeted commitment with the
+// progress fallback (Section 3.2), and their launchers.
+#include "rpd_device.h"
+
+namespace rpd {
+namespace {
+
+// ------------------------------------------------------------ K0 compact --
+
+__global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ mask, int BL, int cap,
+                                                   int32_t* __restrict__ rows, int32_t* __restrict__ n_out,
+                                                   int32_t* __restrict__ dev_status,
+                                                   int32_t* __restrict__ user_status) {
+  __shared__ int wsum[16];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int carry = 0;
+  for (int base = 0; base < BL; base += blockDim.x) {
+    const int i = base + threadIdx.x;
+    const int f = (i < BL && mask[i] != 0) ? 1 : 0;
+    const unsigned long long bal = __ballot(f);
+    const int before = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[wid] = __popcll(bal);
+    __syncthreads();
+    int off = 0, tot = 0;
+    for (int w = 0; w < nw; ++w) {
+      const int c = wsum[w];
+      off += (w < wid) ? c : 0;
+      tot += c;
+    }
+    const int pos = carry + off + before;
+    if (f && pos < cap) rows[pos] = i;
+    carry += tot;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    int st = 0, n = carry;
+    if (n > cap) {
+      st |= 1;
+      n = cap;
+    }
+    *n_out = n;
+    *dev_status = st;
+    if (user_status) *user_status = st;
+  }
+}
+
+// ------------------------------------------------------ scoring (Eq. 2-5) --
+
+__device__ __forceinline__ float stability_score(int k_i, float r_i, int k_max, float w) {
+  return fmaf(-w, r_i, (float)min(k_i, k_max));
+}
+
+__device__ __forceinline__ unsigned route_flags(float c, float s, float theta_h, float theta_c, float theta_s) {
+  const bool high = c >= theta_h;
+  const bool stab = (c >= theta_c) && (c < theta_h) && (s >= theta_s);
+  return (high || stab ? kFlagCandidate : 0u) | (high ? kFlagHigh : 0u) | (stab ? kFlagStable : 0u);
+}
+
+struct ScoreArgs {
+  int K, B, L;
+  float theta_h, theta_c, theta_s, w;
+  int k_max;
+  int32_t* token;
+  float* entropy;
+  float* confidence;
+  int32_t* persistence;
+  float* drop;
+  float* stability;
+  uint8_t* flags;
+  int32_t* layer_argmax;
+  float* layer_conf;
+  float* layer_entropy;
+};
+
+// One workgroup of four waves per masked position. Wave w merges the
+// vocab-tile states of layers w, w+4, ...: each lane folds tiles lane,
+// lane+64, ... in tile order (loads batched four at a time), then a fixed
+// xor butterfly combines the lanes. Wave 0 then evaluates persistence, drop
+// and stability with one lane per layer.
+constexpr int kReduceWaves = 4;
+
+__global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4* __restrict__ partials,
+                                                                     const int32_t* __restrict__ rows,
+                                                                     const int32_t* __restrict__ n_ptr, int nvt,
+                                                                     ScoreArgs a) {
+  __shared__ int ly[64];
+  __shared__ float lc[64], lh[64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int p = blockIdx.x;
+  if (p >= *n_ptr) return;
+  const int pos = rows[p];
+  const int b = pos / a.L, i = pos - b * a.L;
+  const float4 empty = soft_pack(soft_empty());
+  for (int l = wid; l < a.K; l += kReduceWaves) {
+    const float4* src = partials + ((long long)p * a.K + l) * nvt;
+    Soft s = soft_empty();
+    for (int t0 = lane; t0 < nvt; t0 += 64 * 4) {
+      float4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = (t0 + 64 * u < nvt) ? src[t0 + 64 * u] : empty;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) s = soft_merge(s, soft_unpack(v[u]));
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) s = soft_merge(s, soft_shfl_xor(s, m));
+    if (lane == 0) {
+      const float h = fmaxf(logf(s.S) - s.T / s.S, 0.0f);
+      ly[l] = (s.idx == INT_MAX) ? -1 : s.idx;
+      lc[l] = 1.0f / s.S;
+      lh[l] = (s.S != s.S) ? s.S : h;   // keep NaN visible
+    }
+  }
+  __syncthreads();
+  if (wid != 0) return;
+  const int my_y = lane < a.K ? ly[lane] : -1;
+  const float my_c = lane < a.K ? lc[lane] : 0.f;
+  const float my_h = lane < a.K ? lh[lane] : 0.f;
+  const int yK = ly[a.K - 1];
+  const float cK = lc[a.K - 1];
+  const float hK = lh[a.K - 1];
+  // Eq. 2: agreement suffix ending at the final layer
+  const unsigned long long dis = __ballot(lane < a.K && my_y != yK);
+  const int last_dis = dis ? 63 - __clzll(dis) : -1;
+  const int k_i = a.K - 1 - last_dis;
+  // Eq. 3: inside the suffix the final token is each layer's argmax, so its
+  // probability there is that layer's top probability
+  float pk = (lane >= a.K - k_i && lane < a.K) ? my_c : -INFINITY;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) pk = fmaxf(pk, __shfl_xor(pk, m));
+  const float r_i = pk - cK;
+  const float s_i = stability_score(k_i, r_i, a.k_max, a.w);
+  const unsigned fl = route_flags(cK, s_i, a.theta_h, a.theta_c, a.theta_s);
+  const long long o = (long long)b * a.L + i;
+  if (lane == 0) {
+    a.token[o] = yK;
+    a.entropy[o] = hK;
+    a.confidence[o] = cK;
+    a.persistence[o] = k_i;
+    a.drop[o] = r_i;
+    a.stability[o] = s_i;
+    a.flags[o] = (uint8_t)fl;
+  }
+  if (a.layer_argmax && lane < a.K) {
+    const long long ol = ((long long)lane * a.B + b) * a.L + i;
+    a.layer_argmax[ol] = my_y;
+    a.layer_conf[ol] = my_c;
+    a.layer_entropy[ol] = my_h;
+  }
+}
+
+// Scoring from caller-supplied per-layer statistics, one thread per canvas
+// position (same formulas as k_reduce_score, evaluated sequentially).
+__global__ __launch_bounds__(256) void k_gate_score(const uint8_t* __restrict__ mask,
+                                                     const int32_t* __restrict__ l_y,
+                                                     const float* __restrict__ l_c,
+                                                     const float* __restrict__ l_h, ScoreArgs a) {
+  const long long BL = (long long)a.B * a.L;
+  const long long o = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (o >= BL || mask[o] == 0) return;
+  const int yK = l_y[(long long)(a.K - 1) * BL + o];
+  const float cK = l_c[(long long)(a.K - 1) * BL + o];
+  const float hK = l_h[(long long)(a.K - 1) * BL + o];
+  int k_i = 1;
+  float pk = cK;
+  for (int l = a.K - 2; l >= 0; --l) {
+    if (l_y[(long long)l * BL + o] != yK) break;
+    ++k_i;
+    pk = fmaxf(pk, l_c[(long long)l * BL + o]);
+  }
+  const float r_i = pk - cK;
+  const float s_i = stability_score(k_i, r_i, a.k_max, a.w);
+  a.token[o] = yK;
+  a.entropy[o] = hK;
+  a.confidence[o] = cK;
+  a.persistence[o] = k_i;
+  a.drop[o] = r_i;
+  a.stability[o] = s_i;
+  a.flags[o] = (uint8_t)route_flags(cK, s_i, a.theta_h, a.theta_c, a.theta_s);
+}
+
+// --------------------------------------------------- commitment (Sec. 3.2) --
+
+constexpr int kCommitThreads = 1024;
+
+// exclusive prefix sum over the workgroup in thread order (fixed tree order);
+// `total` receives the sum of all values
+template <typename T>
+__device__ __forceinline__ T block_exclusive_scan(T v, T* sh, T& total) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  T x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const T y = __shfl_up(x, o);
+    if (lane >= o) x = x + y;
+  }
+  if (lane == 63) sh[wid] = x;
+  __syncthreads();
+  if (wid == 0) {
+    T s = (lane < nw) ? sh[lane] : T(0);
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const T y = __shfl_up(s, o);
+      if (lane >= o) s = s + y;
+    }
+    if (lane < nw) sh[32 + lane] = s;   // inclusive over waves
+  }
+  __syncthreads();
+  const T wave_before = (wid == 0) ? T(0) : sh[32 + wid - 1];
+  total = sh[32 + nw - 1];
+  const T res = wave_before + x - v;
+  __syncthreads();
+  return res;
+}
+
+struct CommitArgs {
+  int B, L;
+  float beta;
+  int window;
+  uint8_t* commit;
+  int32_t* token;
+  float* entropy;
+  float* confidence;
+  int32_t* persistence;
+  float* drop;
+  float* stability;
+  uint8_t* flags;
+  float* upstream_entropy;
+  int32_t* n_commit;
+};
+
+// One workgroup per sequence. N_i = entropy summed over earlier masked
+// non-candidates; a candidate is committed iff N_i <= beta, which is exactly
+// the left-to-right construction of the paper (every earlier candidate of an
+// accepted position is accepted, so the positions left out before it are the
+// non-candidates; a rejected candidate's sum only grows). E_i (reported) is
+// the entropy over earlier masked positions not committed. Without any
+// commit, the most confident of the first `window` masked positions is
+// committed (lowest index on ties; NaN confidences never win).
+__global__ __launch_bounds__(kCommitThreads) void k_commit(const uint8_t* __restrict__ mask, CommitArgs a) {
+  __shared__ float shf[64];
+  __shared__ int shi[64];
+  __shared__ float red_c[16];
+  __shared__ int red_i[16];
+  const int b = blockIdx.x;
+  const long long base = (long long)b * a.L;
+  float carryN = 0.f, carryE = 0.f;
+  int carryM = 0, ncommit = 0;
+  float best_c = -INFINITY;
+  int best_i = INT_MAX;
+  for (int c0 = 0; c0 < a.L; c0 += blockDim.x) {
+    const int i = c0 + threadIdx.x;
+    const bool in = i < a.L;
+    const bool masked = in && mask[base + i] != 0;
+    const unsigned fl = masked ? a.flags[base + i] : 0u;
+    const bool cand = (fl & kFlagCandidate) != 0;
+    const float H = masked ? a.entropy[base + i] : 0.f;
+    float totN, totE;
+    int totM;
+    const float N_i = carryN + block_exclusive_scan<float>((masked && !cand) ? H : 0.f, shf, totN);
+    const bool com = masked && cand && (N_i <= a.beta);
+    const float E_i = carryE + block_exclusive_scan<float>((masked && !com) ? H : 0.f, shf, totE);
+    const int rank = carryM + block_exclusive_scan<int>(masked ? 1 : 0, shi, totM);
+    int ncom_chunk;
+    (void)block_exclusive_scan<int>(com ? 1 : 0, shi, ncom_chunk);
+    if (in) {
+      const long long o = base + i;
+      if (masked) {
+        a.commit[o] = com ? 1 : 0;
+        a.flags[o] = (uint8_t)(fl | (com ? kFlagCommitted : 0u));
+        a.upstream_entropy[o] = E_i;
+        if (rank < a.window) {
+          float cv = a.confidence[o];
+          cv = (cv != cv) ? -INFINITY : cv;
+          if (cv > best_c || (cv == best_c && i < best_i)) {
+            best_c = cv;
+            best_i = i;
+          }
+        }
+      } else {
+        a.commit[o] = 0;
+        a.token[o] = -1;
+        a.entropy[o] = 0.f;
+        a.confidence[o] = 0.f;
+        a.persistence[o] = 0;
+        a.drop[o] = 0.f;
+        a.stability[o] = 0.f;
+        a.flags[o] = 0;
+        a.upstream_entropy[o] = 0.f;
+      }
+    }
+    carryN += totN;
+    carryE += totE;
+    carryM += totM;
+    ncommit += ncom_chunk;
+  }
+  if (ncommit == 0 && carryM > 0) {
+    // workgroup argmax of (confidence, -index) over the window
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const float oc = __shfl_xor(best_c, m);
+      const int oi = __shfl_xor(best_i, m);
+      if (oc > best_c || (oc == best_c && oi < best_i)) {
+        best_c = oc;
+        best_i = oi;
+      }
+    }
+    if (lane == 0) {
+      red_c[wid] = best_c;
+      red_i[wid] = best_i;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float bc = red_c[0];
+      int bi = red_i[0];
+      for (int w = 1; w < nw; ++w)
+        if (red_c[w] > bc || (red_c[w] == bc && red_i[w] < bi)) {
+          bc = red_c[w];
+          bi = red_i[w];
+        }
+      if (bi != INT_MAX) {   // the window always holds a masked position here
+        const long long o = base + bi;
+        a.commit[o] = 1;
+        a.flags[o] = (uint8_t)(a.flags[o] | kFlagCommitted | kFlagFallback);
+        ncommit = 1;
+      }
+    }
+  }
+  if (threadIdx.x == 0) a.n_commit[b] = ncommit;
+}
+
+ScoreArgs score_args(const Launch& a) {
+  ScoreArgs s;
+  s.K = a.K;
+  s.B = a.B;
+  s.L = a.L;
+  s.theta_h = a.theta_h;
+  s.theta_c = a.theta_c;
+  s.theta_s = a.theta_s;
+  s.w = a.w;
+  s.k_max = a.k_max;
+  s.token = a.token;
+  s.entropy = a.entropy;
+  s.confidence = a.confidence;
+  s.persistence = a.persistence;
+  s.drop = a.drop;
+  s.stability = a.stability;
+  s.flags = a.flags;
+  s.layer_argmax = a.layer_argmax;
+  s.layer_conf = a.layer_conf;
+  s.layer_entropy = a.layer_entropy;
+  return s;
+}
+
+CommitArgs commit_args(const Launch& a) {
+  CommitArgs c;
+  c.B = a.B;
+  c.L = a.L;
+  c.beta = a.beta;
+  c.window = a.window;
+  c.commit = a.commit;
+  c.token = a.token;
+  c.entropy = a.entropy;
+  c.confidence = a.confidence;
+  c.persistence = a.persistence;
+  c.drop = a.drop;
+  c.stability = a.stability;
+  c.flags = a.flags;
+  c.upstream_entropy = a.upstream_entropy;
+  c.n_commit = a.n_commit;
+  return c;
+}
+
+}  // namespace
+
+hipError_t launch_compact(const Launch& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, a.mask, a.B * a.L, a.max_masked, a.rows, a.n_masked,
+                     a.dev_status, a.user_status);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_score(const Launch& a, hipStream_t s) {
+  if (a.max_masked <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_reduce_score, dim3(a.max_masked), dim3(64 * kReduceWaves), 0, s, a.partials, a.rows,
+                     a.n_masked, a.plan.nvt, score_args(a));
+  return hipGetLastError();
+}
+
+int commit_threads(int L) {
+  const int t = ((L + 63) / 64) * 64;
+  return t < kCommitThreads ? t : kCommitThreads;
+}
+
+hipError_t launch_commit(const Launch& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_commit, dim3(a.B), dim3(commit_threads(a.L)), 0, s, a.mask, commit_args(a));
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_commit(const Launch& a, const int32_t* l_y, const float* l_c, const float* l_h,
+                              hipStream_t s) {
+  const long long BL = (long long)a.B * a.L;
+  hipLaunchKernelGGL(k_gate_score, dim3((unsigned)((BL + 255) / 256)), dim3(256), 0, s, a.mask, l_y, l_c, l_h,
+                     score_args(a));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_commit, dim3(a.B), dim3(commit_threads(a.L)), 0, s, a.mask, commit_args(a));
+  return hipGetLastError();
+}
+
+}  // namespace rpd

@@ -55,6 +55,16 @@ def test_workspace_size():
     assert rpd.workspace_size(4, 1, 256, 4096, 126464, 7) == 0
 
 
+def test_projection_variant_thresholds():
+    pv = lambda n, dt=rpd.DTYPE_BF16: rpd.projection_variant(4, 1, 256, 4096, 126464, dt, max_masked=n)  # noqa: E731
+    assert [pv(n) for n in (1, 8, 9, 16, 17, 48, 49, 64, 256)] == \
+        ["bf16_r32", "bf16_r32", "bf16_r64", "bf16_r64", "bf16_m32", "bf16_m32", "bf16_big", "bf16_big", "bf16_big"]
+    assert pv(8, rpd.DTYPE_F32) == "f32" and pv(256, rpd.DTYPE_F32) == "f32"
+    assert pv(-1) == "bf16_big"          # -1 plans for every position masked
+    with pytest.raises(rpd.RpdError):
+        rpd.projection_variant(0, 1, 256, 4096, 126464, rpd.DTYPE_BF16)
+
+
 def _call(prob, params, outs, ws=256, ws_bytes=1 << 40):
     L = rpd.lib()
     s = L.rpd_score_commit(ctypes.byref(prob) if prob is not None else None,

@@ -58,13 +58,14 @@ def test_tiny_f32_calibrated(seed, pname):
 # ------------------------------------------------- bf16, several variants --
 
 BF16_CASES = [
-    # name, overrides, seed; rows = K * masked
-    ("r32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
-    ("r64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10, masked_frac=None), 12),
-    ("m32_one_tile", dict(B=1, L=40, K=4, d=4104, V=2500, n_masked=20, masked_frac=None), 15),
-    ("m32_two_tiles", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=20, masked_frac=None), 16),
-    ("big_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
-    ("big_row_split", dict(B=4, L=600, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
+    # name (the projection variant the case runs, then what it exercises), overrides, seed;
+    # rows = K * masked
+    ("bf16_r32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
+    ("bf16_r64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10, masked_frac=None), 12),
+    ("bf16_m32_one_tile", dict(B=1, L=40, K=4, d=4104, V=2500, n_masked=20, masked_frac=None), 15),
+    ("bf16_m32_two_tiles", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=20, masked_frac=None), 16),
+    ("bf16_big_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
+    ("bf16_big_row_split", dict(B=4, L=600, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
 ]
 
 
@@ -75,6 +76,8 @@ def test_bf16_variants(name, ov, seed, sharp):
     if sharp == "calibrated":
         base = base.with_(sharp=("calibrated",), unstable_frac=0.3)
     w = make_workload(base, seed)
+    variant = rpd.projection_variant(base.K, base.B, base.L, base.d, base.V, rpd.DTYPE_BF16, max_masked=w.n_masked)
+    assert name.startswith(variant), (name, variant)
     for P in (O.strict(base.K, 1.0), O.LLADA, O.DREAM):
         _check(w, P)
 
