@@ -5,47 +5,36 @@
 namespace rpd {
 namespace {
 
-// Compute-bound row counts: a GEMM tile of 256 vocabulary rows x 256
-// projected rows with both operands staged in LDS by direct global->LDS
-// loads (global_load_lds_dwordx4: each lane's 16 bytes land at the wave's
-// LDS base + 16 * lane), so no registers hold loads in flight and three
-// 32-wide k-chunks can be in flight per workgroup in a four-stage ring. A
-// load instruction covers 16 rows x 64 bytes; the 16-byte pieces of row r
-// are stored XOR-swizzled by (r >> 2) & 3 (chosen through which global
-// piece each lane fetches), which makes the MFMA fragment reads free of
-// bank conflicts. Four waves in a 2 x 2 layout each compute 128 x 128 with
-// v_mfma_f32_32x32x16_bf16 (256 accumulators per lane, one wave per SIMD).
+// A GEMM tile of 256 vocabulary rows x 256 projected rows over the full
+// hidden dimension, four waves in a 2 x 2 layout, each computing 128 x 128
+// with v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane in AGPRs,
+// one wave per SIMD).
+//
+// Operands move global -> registers -> LDS -> MFMA fragments. A 32-wide
+// k-chunk of both operands (256 rows x 64 bytes each) is loaded into
+// registers two chunks ahead (16 B per lane, a wave instruction covering 16
+// rows x 64 bytes), written to one of two LDS stages, and read back as MFMA
+// fragments. Within a tile row the four 16-byte pieces are stored XOR-
+// swizzled by (row >> 2) & 3 (chosen through which global piece each lane
+// fetches), so the fragment reads are free of bank conflicts.
+//
+// Plain loads into registers rather than direct global->LDS loads: with one
+// wave per SIMD, direct loads sustain about 17 B/clk per CU, below the
+// 32 B/clk this tile needs at full MFMA rate, and being opaque to the
+// compiler's scheduler they cannot be spread between MFMAs; register loads
+// sustain about 26 B/clk and interleave.
+//
+// Per chunk c (stage c & 1), the instruction stream is fixed with scheduling
+// groups so that one memory instruction issues between consecutive MFMAs:
+//   first half:  MFMAs of k-step (c,0), interleaved with the fragment reads
+//                of (c,1), the LDS writes of chunk c+1 and the global loads
+//                of chunk c+3;
+//   barrier:     publishes chunk c+1 and frees stage c & 1;
+//   second half: MFMAs of (c,1), interleaved with the fragment reads of
+//                (c+1,0).
 namespace big {
-constexpr int TV = kBigTileVocab, TR = kBigTileRows, KC = 32, NSTG = 4;
-constexpr int LOADS = 8;   // direct loads per wave per chunk: 4 for W_U rows, 4 for hidden rows
-
-// One direct global->LDS load of 16 bytes per lane (lane l writes LDS bytes
-// [lds + 16 l, +16)). Issued through inline asm so that the compiler's
-// wait-count insertion does not treat it as an LDS store that every later
-// LDS read must wait for; the kernel orders these loads with explicit
-// vmcnt waits and barriers instead. No compiler-visible vector-memory load
-// may be in flight where those explicit waits are relied on.
-__device__ __forceinline__ void dma16(const uint16_t* gptr, const void* lds) {
-  const uint32_t lds_addr =
-      __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(__attribute__((address_space(3))) const void*)lds);
-  asm volatile(
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, off"
-      :
-      : "v"(gptr), "s"(lds_addr)
-      : "memory", "m0");
-}
-
-__device__ __forceinline__ void vmcnt_wait_loads(int outstanding_chunks) {
-  // s_waitcnt vmcnt(outstanding_chunks * LOADS); expcnt and lgkmcnt left unconstrained
-  switch (outstanding_chunks) {
-    case 0: __builtin_amdgcn_s_waitcnt(0x0F70 | 0); break;
-    case 1: __builtin_amdgcn_s_waitcnt(0x0F70 | LOADS); break;
-    case 2: __builtin_amdgcn_s_waitcnt((0x0F70 | ((2 * LOADS) & 15)) | (((2 * LOADS) >> 4) << 14)); break;
-    default: __builtin_amdgcn_s_waitcnt(0); break;
-  }
-}
+constexpr int TV = kBigTileVocab, TR = kBigTileRows, KC = 32;
+constexpr int D = 2;   // chunks in flight in registers
 }  // namespace big
 
 __global__ __launch_bounds__(256) void k_proj_bf16_big(
@@ -53,15 +42,12 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
     int nvt, int nrt, int split_rows) {
   using namespace big;
-  static_assert(NSTG == 4 && 2 * LOADS < 64, "wait counts below assume three chunks in flight");
-  // one LDS object per ring stage: the compiler then knows that reads of the
-  // stage being multiplied do not alias the direct loads filling another
-  // stage, and does not wait for those loads before the reads
-  __shared__ __attribute__((aligned(16))) uint16_t sa0[TV][KC], sa1[TV][KC], sa2[TV][KC], sa3[TV][KC];
-  __shared__ __attribute__((aligned(16))) uint16_t sb0[TR][KC], sb1[TR][KC], sb2[TR][KC], sb3[TR][KC];
+  static_assert(TV == 256 && TR == 256 && D == 2, "wave layout and register ring below assume these");
+  __shared__ __attribute__((aligned(16))) uint16_t sa0[TV][KC], sa1[TV][KC];
+  __shared__ __attribute__((aligned(16))) uint16_t sb0[TR][KC], sb1[TR][KC];
   __shared__ float4 red[2][TR];
-#define RPD_SA(S) ((S) == 0 ? sa0 : (S) == 1 ? sa1 : (S) == 2 ? sa2 : sa3)
-#define RPD_SB(S) ((S) == 0 ? sb0 : (S) == 1 ? sb1 : (S) == 2 ? sb2 : sb3)
+#define RPD_SA(S) ((S) == 0 ? sa0 : sa1)
+#define RPD_SB(S) ((S) == 0 ? sb0 : sb1)
 
   int rt, vt;
   if (!map_job(blockIdx.x, nvt, nrt, split_rows, rt, vt)) return;
@@ -73,21 +59,22 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wv = wid & 1, wr = wid >> 1;
 
-  // direct-load sources: instruction j of this wave covers tile rows
-  // 64*wid + 16*j .. +16; lane l fills LDS piece (l & 3) of row (l >> 2) with
-  // the global piece (l & 3) ^ swizzle(row)
+  // load sources: instruction u of this wave covers tile rows
+  // 64*wid + 16*u .. +16; lane l holds LDS piece (l & 3) of row (l >> 2),
+  // fetched from the global piece (l & 3) ^ swizzle(row)
   long long ga[4], gb[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int tr = 64 * wid + 16 * j + (lane >> 2);
+  for (int u = 0; u < 4; ++u) {
+    const int tr = 64 * wid + 16 * u + (lane >> 2);
     const int piece = (lane & 3) ^ ((tr >> 2) & 3);
-    ga[j] = (long long)min(vb + tr, ve - 1) * d + piece * 8;
+    ga[u] = (long long)min(vb + tr, ve - 1) * d + piece * 8;
     const int r = r0 + tr < R ? r0 + tr : r0;   // padding rows re-read a real row; discarded at the end
     const int p = r / K, l = r - p * K;
     const int pos = rows[p];
     const int b = pos / L, i = pos - b * L;
-    gb[j] = (((long long)l * B + b) * L + i) * (long long)d + piece * 8;
+    gb[u] = (((long long)l * B + b) * L + i) * (long long)d + piece * 8;
   }
+  const int srow = lane >> 2, scol = (lane & 3) * 8;
   // fragment reads: lane reads row base + (lane & 31), logical piece 2s + (lane >> 5)
   const int swl = ((lane & 31) >> 2) & 3;
   const int fcol0 = 8 * ((0 + (lane >> 5)) ^ swl), fcol1 = 8 * ((2 + (lane >> 5)) ^ swl);
@@ -99,80 +86,109 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[mv][nb][q] = 0.f;
+  u32x4 ld[D][8];
+  u32x4 fa0[4], fb0[4], fa1[4], fb1[4];
 
-#define RPD_BIG_ISSUE(chunk, stage)                                                                      \
-  do {                                                                                                   \
-    _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                                  \
-      dma16(w_u + ga[u_] + (chunk) * KC, &RPD_SA(stage)[64 * wid + 16 * u_][0]);                       \
-      dma16(hidden + gb[u_] + (chunk) * KC, &RPD_SB(stage)[64 * wid + 16 * u_][0]);                    \
-    }                                                                                                    \
+#define RPD_LOAD(slot, chunk)                                                                             \
+  do {                                                                                                    \
+    const long long k0_ = (long long)(chunk) * KC;                                                        \
+    _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                                   \
+      ld[slot][u_] = *reinterpret_cast<const u32x4*>(w_u + ga[u_] + k0_);                                 \
+      ld[slot][4 + u_] = *reinterpret_cast<const u32x4*>(hidden + gb[u_] + k0_);                          \
+    }                                                                                                     \
   } while (0)
-#define RPD_BIG_COMPUTE(stage)                                                                            \
-  do {                                                                                                   \
-    const uint16_t(*pa_)[KC] = RPD_SA(stage);                                                            \
-    const uint16_t(*pb_)[KC] = RPD_SB(stage);                                                            \
-    _Pragma("unroll") for (int s_ = 0; s_ < 2; ++s_) {                                                  \
-      const int fc_ = s_ ? fcol1 : fcol0;                                                                \
-      u32x4 fa_[4], fb_[4];                                                                              \
-      _Pragma("unroll") for (int m = 0; m < 4; ++m) {                                                   \
-        fa_[m] = *reinterpret_cast<const u32x4*>(&pa_[128 * wv + 32 * m + (lane & 31)][fc_]);           \
-        fb_[m] = *reinterpret_cast<const u32x4*>(&pb_[128 * wr + 32 * m + (lane & 31)][fc_]);           \
-      }                                                                                                  \
-      _Pragma("unroll") for (int mv = 0; mv < 4; ++mv)                                                  \
-      _Pragma("unroll") for (int nb = 0; nb < 4; ++nb)                                                  \
-        acc[mv][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa_[mv]),       \
-                                                               __builtin_bit_cast(bf16x8, fb_[nb]),       \
-                                                               acc[mv][nb], 0, 0, 0);                    \
-    }                                                                                                    \
+#define RPD_STORE(slot, stage)                                                                            \
+  do {                                                                                                    \
+    _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                                   \
+      *reinterpret_cast<u32x4*>(&RPD_SA(stage)[64 * wid + 16 * u_ + srow][scol]) = ld[slot][u_];         \
+      *reinterpret_cast<u32x4*>(&RPD_SB(stage)[64 * wid + 16 * u_ + srow][scol]) = ld[slot][4 + u_];     \
+    }                                                                                                     \
+  } while (0)
+#define RPD_FRAGS(FA, FB, stage, kstep)                                                                   \
+  do {                                                                                                    \
+    const int fc_ = (kstep) ? fcol1 : fcol0;                                                              \
+    _Pragma("unroll") for (int m_ = 0; m_ < 4; ++m_) {                                                   \
+      FA[m_] = *reinterpret_cast<const u32x4*>(&RPD_SA(stage)[128 * wv + 32 * m_ + (lane & 31)][fc_]);   \
+      FB[m_] = *reinterpret_cast<const u32x4*>(&RPD_SB(stage)[128 * wr + 32 * m_ + (lane & 31)][fc_]);   \
+    }                                                                                                     \
+  } while (0)
+#define RPD_MMA(FA, FB)                                                                                   \
+  do {                                                                                                    \
+    _Pragma("unroll") for (int mv_ = 0; mv_ < 4; ++mv_)                                                  \
+    _Pragma("unroll") for (int nb_ = 0; nb_ < 4; ++nb_)                                                  \
+      acc[mv_][nb_] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, FA[mv_]),        \
+                                                               __builtin_bit_cast(bf16x8, FB[nb_]),        \
+                                                               acc[mv_][nb_], 0, 0, 0);                   \
+  } while (0)
+  // one chunk c, held in stage ST; its successor goes to stage ST^1 from
+  // register slot SL, which is then refilled with chunk c+1+D. Chunks past
+  // the end repeat the last one (loaded and staged, never multiplied).
+#define RPD_CHUNK(c, ST, SL)                                                                              \
+  do {                                                                                                    \
+    __builtin_amdgcn_sched_barrier(0);                                                                    \
+    RPD_FRAGS(fa1, fb1, ST, 1);                                                                           \
+    RPD_STORE(SL, (ST) ^ 1);                                                                              \
+    RPD_LOAD(SL, min((c) + 1 + D, nchf - 1));                                                             \
+    RPD_MMA(fa0, fb0);                                                                                    \
+    _Pragma("unroll") for (int g_ = 0; g_ < 8; ++g_) {                                                   \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */                                       \
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* LDS read */                                   \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */                                       \
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0); /* LDS write */                                  \
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0); /* global load */                                \
+    }                                                                                                     \
+    __builtin_amdgcn_sched_barrier(0);                                                                    \
+    __syncthreads();                                                                                      \
+    __builtin_amdgcn_sched_barrier(0);                                                                    \
+    RPD_FRAGS(fa0, fb0, (ST) ^ 1, 0);                                                                     \
+    RPD_MMA(fa1, fb1);                                                                                    \
+    _Pragma("unroll") for (int g_ = 0; g_ < 8; ++g_) {                                                   \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                                  \
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                                  \
+    }                                                                                                     \
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                                                    \
+    __builtin_amdgcn_sched_barrier(0);                                                                    \
   } while (0)
 
   const int nchf = d / KC;
   if (nchf > 0) {
 #pragma unroll
-    for (int j = 0; j < NSTG - 1; ++j) RPD_BIG_ISSUE(min(j, nchf - 1), j);
-    vmcnt_wait_loads(NSTG - 2);
+    for (int j = 0; j < D; ++j) RPD_LOAD(j, min(j, nchf - 1));
+    RPD_STORE(0, 0);
+    RPD_LOAD(0, min(D, nchf - 1));
     __syncthreads();
-    // unrolled by NSTG so that every stage is a compile-time choice; a stage
-    // refilled in a trip was consumed in the previous one (all waves passed
-    // the barrier since); chunks past the end repeat the last one
-    const int nmain = (nchf / NSTG) * NSTG;
-    for (int c0 = 0; c0 < nmain; c0 += NSTG) {
-#pragma unroll
-      for (int j = 0; j < NSTG; ++j) {
-        RPD_BIG_ISSUE(min(c0 + j + NSTG - 1, nchf - 1), (j + NSTG - 1) % NSTG);
-        RPD_BIG_COMPUTE(j);
-        vmcnt_wait_loads(NSTG - 2);   // chunk c+1 has landed (this wave's share)
-        __syncthreads();              // ... and every wave's share
-      }
+    RPD_FRAGS(fa0, fb0, 0, 0);
+    int c = 0;
+    for (; c + 2 <= nchf; c += 2) {
+      RPD_CHUNK(c, 0, 1);
+      RPD_CHUNK(c + 1, 1, 0);
     }
-    const int rem = nchf - nmain;   // < NSTG chunks left, already in stages 0 .. rem-1
-#pragma unroll
-    for (int j = 0; j < NSTG - 1; ++j)
-      if (j < rem) {
-        RPD_BIG_COMPUTE(j);
-        vmcnt_wait_loads(0);
-        __syncthreads();
-      }
-    vmcnt_wait_loads(0);
-    __syncthreads();
+    if (c < nchf) RPD_CHUNK(c, 0, 1);
   }
-  if (d % KC != 0) {   // partial last chunk through registers, zero-filled past d
-    const int k0 = nchf * KC;
+  if (d % KC != 0) {   // partial last chunk, zero-filled past d (d % 8 == 0: a piece is all in or all out)
+    __syncthreads();   // every wave is done with both stages
+    const long long k0 = (long long)nchf * KC;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int tr = 64 * wid + 16 * j + (lane >> 2);
+    for (int u = 0; u < 4; ++u) {
+      const int tr = 64 * wid + 16 * u + srow;
       const int piece = (lane & 3) ^ ((tr >> 2) & 3);
       const bool in = k0 + piece * 8 < d;
-      const u32x4 va = in ? *reinterpret_cast<const u32x4*>(w_u + ga[j] + k0) : u32x4{0u, 0u, 0u, 0u};
-      const u32x4 vbv = in ? *reinterpret_cast<const u32x4*>(hidden + gb[j] + k0) : u32x4{0u, 0u, 0u, 0u};
-      *reinterpret_cast<u32x4*>(&sa0[tr][(lane & 3) * 8]) = va;
-      *reinterpret_cast<u32x4*>(&sb0[tr][(lane & 3) * 8]) = vbv;
+      const u32x4 va = in ? *reinterpret_cast<const u32x4*>(w_u + ga[u] + k0) : u32x4{0u, 0u, 0u, 0u};
+      const u32x4 vh = in ? *reinterpret_cast<const u32x4*>(hidden + gb[u] + k0) : u32x4{0u, 0u, 0u, 0u};
+      *reinterpret_cast<u32x4*>(&sa0[tr][scol]) = va;
+      *reinterpret_cast<u32x4*>(&sb0[tr][scol]) = vh;
     }
     __syncthreads();
-    RPD_BIG_COMPUTE(0);
+    RPD_FRAGS(fa0, fb0, 0, 0);
+    RPD_MMA(fa0, fb0);
+    RPD_FRAGS(fa1, fb1, 0, 1);
+    RPD_MMA(fa1, fb1);
   }
-#undef RPD_BIG_ISSUE
-#undef RPD_BIG_COMPUTE
+#undef RPD_CHUNK
+#undef RPD_MMA
+#undef RPD_FRAGS
+#undef RPD_STORE
+#undef RPD_LOAD
 #undef RPD_SA
 #undef RPD_SB
 

@@ -16,7 +16,7 @@ enum ProjVariant {
   PROJ_BF16_R64 = 1,   // 64 rows per tile, 8 waves x 64 vocab
   PROJ_BF16_M32 = 2,   // up to 192 rows: 32x32 MFMA, 128 rows per tile, 8 waves x 64 vocab
   PROJ_F32 = 3,        // fp32 inputs: vector ALU, 16 rows x 64 vocab
-  PROJ_BF16_BIG = 4,   // compute-bound: 256 x 256 tiles, both operands through LDS
+  PROJ_BF16_BIG = 4,   // compute-bound: 256 x 256 tiles, both operands staged through LDS
 };
 
 // tile of the large-row variant: vocabulary rows x projected rows
