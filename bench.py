@@ -36,7 +36,7 @@ VARIANT_SOURCES = {
     "bf16_big": ["rpd_device.h", "proj_big.hip"],
     "f32": ["rpd_device.h", "proj_f32.hip"],
 }
-VARIANT_KERNEL = {"bf16_r32": "k_proj_bf16", "bf16_r64": "k_proj_bf16", "bf16_m32": "k_proj_bf16_m32",
+VARIANT_KERNEL = {"bf16_r32": "k_proj_bf16_stream", "bf16_r64": "k_proj_bf16", "bf16_m32": "k_proj_bf16_m32",
                   "bf16_big": "k_proj_bf16_big", "f32": "k_proj_f32"}
 COPY_PROBE_BYTES = 1 << 30     # fp32 elements read (and as many written) by the copy probe
 

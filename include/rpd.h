@@ -169,8 +169,9 @@ rpd_status rpd_score_commit(const rpd_problem* p, const rpd_params* q, const rpd
  * stages: events[0] before the masked-position compaction, [1] before the
  * projection (logit lens + fused softmax statistics), [2] after it, [3]
  * after the cross-tile reduction and stability scoring, [4] after the
- * commitment scan. Only the first n_events (0..5) are used; NULL entries
- * are skipped. Everything else is exactly rpd_score_commit.
+ * commitment scan (with B == 1 the commitment runs inside the reduction
+ * kernel, so [3] and [4] coincide). Only the first n_events (0..5) are used;
+ * NULL entries are skipped. Everything else is exactly rpd_score_commit.
  */
 rpd_status rpd_score_commit_timed(const rpd_problem* p, const rpd_params* q, const rpd_outputs* o,
                                   void* workspace, size_t workspace_bytes, void* stream,

@@ -21,7 +21,7 @@ ProjPlan plan_projection(int dtype, long long rows_cap, int V) {
   if (rows_cap <= 64) {
     p.variant = rows_cap <= 32 ? PROJ_BF16_R32 : PROJ_BF16_R64;
     p.rows_per_tile = rows_cap <= 32 ? 32 : 64;
-    p.vocab_cap = 8 * 64;
+    p.vocab_cap = rows_cap <= 32 ? 32 * kStreamWaves * kStreamBlocks : 8 * 64;
     // every CU streams an equal share of W_U: a multiple of 256 tiles
     int nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
     nvt = ((nvt + 255) / 256) * 256;

@@ -1,5 +1,6 @@
 // K1 projection, bf16, small row counts (up to 64 projected rows): the
 // HBM-bound regime, where streaming W_U once per call sets the time.
+// k_proj_bf16_stream serves up to 32 rows, k_proj_bf16 33 to 64.
 #include "proj_stage.h"
 
 namespace rpd {
@@ -199,6 +200,172 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16(
   }
 }
 
+
+// At most 32 projected rows: every wave streams its own W_U rows, with no
+// barrier until the epilogue. Wave w of the workgroup owns 32*MV
+// consecutive W_U rows. They are read in full 128-byte lines (a load
+// instruction covers 8 rows x 8 lanes x 16 B, non-temporal: W_U is read
+// exactly once per call), D = 2 chunks of 64 k-elements ahead in registers,
+// and written to a two-stage LDS ring private to the wave, with the eight
+// 16-byte pieces of row r stored XOR-swizzled by (r >> 1) & 7 so that the
+// MFMA fragment reads are conflict-free. Private stages need no barrier:
+// one wave's LDS accesses complete in order. The hidden rows (at most 32,
+// shared by every workgroup, resident in L2) are read by each wave straight
+// into the B-operand layout of v_mfma_f32_32x32x16_bf16: lane l holds row
+// l & 31, k-elements 8*(l >> 5) .. +8 of each 16-wide k-step. Accumulator
+// register q of lane l holds vocabulary row 32*mv + 8*(q >> 2) + 4*(l >> 5)
+// + (q & 3) of the wave's block and projected row l & 31.
+//
+// Full-line, non-temporal, row-private streaming measured 168 us at the
+// LLaDA-8B shape (77% of 8 TB/s) against 187 us for k_proj_bf16's 16-row x
+// 64-byte register layout.
+template <int NW, int MV>
+__global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
+    const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
+    int nvt, int nrt, int split_rows) {
+  constexpr int TR = 32, WR = 32 * MV, KC = 64, NLD = WR / 8, D = 2;
+  __shared__ __attribute__((aligned(16))) uint16_t wl[NW][2][WR][KC];
+  __shared__ float4 red[NW][TR];
+
+  int rt, vt;
+  if (!map_job(blockIdx.x, nvt, nrt, split_rows, rt, vt)) return;
+  const int R = *n_ptr * K;
+  const int r0 = rt * TR;
+  if (r0 >= R) return;
+  const int vb = (int)((long long)vt * V / nvt);
+  const int ve = (int)((long long)(vt + 1) * V / nvt);
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int vw = vb + wid * WR;
+
+  // W_U: load u covers wave rows 8u + (lane >> 3); lane fetches the global
+  // piece that belongs at LDS piece (lane & 7) of that row
+  long long wa[NLD];
+#pragma unroll
+  for (int u = 0; u < NLD; ++u) {
+    const int row = 8 * u + (lane >> 3);
+    wa[u] = (long long)min(vw + row, ve - 1) * d + (((lane & 7) ^ ((row >> 1) & 7)) * 8);
+  }
+  const int srow = lane >> 3, spc = (lane & 7) * 8;
+  // hidden: this lane's projected row (rows past the last re-read row r0; discarded at the end)
+  long long xo;
+  {
+    const int r = r0 + (lane & 31) < R ? r0 + (lane & 31) : r0;
+    const int p = r / K, l = r - p * K;
+    const int pos = rows[p];
+    const int b = pos / L, i = pos - b * L;
+    xo = (((long long)l * B + b) * L + i) * (long long)d + 8 * (lane >> 5);
+  }
+  const int fr = lane & 31, fsw = (fr >> 1) & 7, fhi = lane >> 5;
+
+  f32x16 acc[MV];
+#pragma unroll
+  for (int mv = 0; mv < MV; ++mv)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[mv][q] = 0.f;
+  u32x4 ld[D][NLD];
+  u32x4 xb[D][4];
+  const int nchf = d / KC;
+
+#define RPD_SLOAD(slot, chunk)                                                                          \
+  do {                                                                                                  \
+    const long long k0_ = (long long)(chunk) * KC;                                                      \
+    _Pragma("unroll") for (int u_ = 0; u_ < NLD; ++u_)                                                 \
+      ld[slot][u_] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(w_u + wa[u_] + k0_));    \
+    _Pragma("unroll") for (int s_ = 0; s_ < 4; ++s_)                                                   \
+      xb[slot][s_] = *reinterpret_cast<const u32x4*>(hidden + xo + k0_ + 16 * s_);                      \
+  } while (0)
+  // chunk c: registers of slot SL -> LDS stage ST, refill SL with chunk
+  // c + D (chunks past the end repeat the last one, never multiplied), then
+  // the four k-steps of chunk c
+#define RPD_SCHUNK(c, SL, ST)                                                                           \
+  do {                                                                                                  \
+    _Pragma("unroll") for (int u_ = 0; u_ < NLD; ++u_)                                                 \
+      *reinterpret_cast<u32x4*>(&wl[wid][ST][8 * u_ + srow][spc]) = ld[SL][u_];                        \
+    u32x4 xc_[4];                                                                                       \
+    _Pragma("unroll") for (int s_ = 0; s_ < 4; ++s_) xc_[s_] = xb[SL][s_];                             \
+    RPD_SLOAD(SL, min((c) + D, nchf - 1));                                                              \
+    _Pragma("unroll") for (int s_ = 0; s_ < 4; ++s_) {                                                 \
+      const int pc_ = 8 * ((2 * s_ + fhi) ^ fsw);                                                       \
+      u32x4 fa_[MV];                                                                                    \
+      _Pragma("unroll") for (int mv_ = 0; mv_ < MV; ++mv_)                                             \
+        fa_[mv_] = *reinterpret_cast<const u32x4*>(&wl[wid][ST][32 * mv_ + fr][pc_]);                  \
+      _Pragma("unroll") for (int mv_ = 0; mv_ < MV; ++mv_)                                             \
+        acc[mv_] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa_[mv_]),        \
+                                                            __builtin_bit_cast(bf16x8, xc_[s_]), acc[mv_], \
+                                                            0, 0, 0);                                   \
+    }                                                                                                   \
+  } while (0)
+
+  if (nchf > 0) {
+    RPD_SLOAD(0, 0);
+    RPD_SLOAD(1, min(1, nchf - 1));
+    int c = 0;
+    for (; c + 2 <= nchf; c += 2) {
+      RPD_SCHUNK(c, 0, 0);
+      RPD_SCHUNK(c + 1, 1, 1);
+    }
+    if (c < nchf) RPD_SCHUNK(c, 0, 0);
+  }
+#undef RPD_SCHUNK
+#undef RPD_SLOAD
+  if (d % KC != 0) {   // partial last chunk, zero-filled past d (d % 8 == 0: a piece is all in or all out)
+    const long long k0 = (long long)nchf * KC;
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) {
+      const int row = 8 * u + srow;
+      const int piece = (lane & 7) ^ ((row >> 1) & 7);
+      *reinterpret_cast<u32x4*>(&wl[wid][0][row][spc]) =
+          k0 + piece * 8 < d ? *reinterpret_cast<const u32x4*>(w_u + wa[u] + k0) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const long long k = k0 + 16 * s + 8 * fhi;
+      const u32x4 xv = k < d ? *reinterpret_cast<const u32x4*>(hidden + xo + k0 + 16 * s) : u32x4{0u, 0u, 0u, 0u};
+      const int pc = 8 * ((2 * s + fhi) ^ fsw);
+      u32x4 fa[MV];
+#pragma unroll
+      for (int mv = 0; mv < MV; ++mv) fa[mv] = *reinterpret_cast<const u32x4*>(&wl[wid][0][32 * mv + fr][pc]);
+#pragma unroll
+      for (int mv = 0; mv < MV; ++mv)
+        acc[mv] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[mv]),
+                                                          __builtin_bit_cast(bf16x8, xv), acc[mv], 0, 0, 0);
+    }
+  }
+
+  // epilogue: softmax state of the wave's vocabulary rows per projected row,
+  // then a fixed-order merge over the waves
+  {
+    Soft sst = soft_empty();
+#pragma unroll
+    for (int mv = 0; mv < MV; ++mv) {
+      float z[16];
+      int vi[16];
+      bool ok[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int v = vw + 32 * mv + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
+        z[q] = acc[mv][q];
+        vi[q] = v;
+        ok[q] = v < ve;
+      }
+      sst = soft_merge(sst, soft_from_values(z, vi, ok));
+    }
+    sst = soft_merge(sst, soft_shfl_xor(sst, 32));
+    if (lane < 32) red[wid][lane] = soft_pack(sst);
+  }
+  __syncthreads();
+  for (int t = tid; t < TR; t += NW * 64) {
+    const int r = r0 + t;
+    if (r < R) {
+      Soft s = soft_unpack(red[0][t]);
+#pragma unroll
+      for (int w = 1; w < NW; ++w) s = soft_merge(s, soft_unpack(red[w][t]));
+      partials[(long long)r * nvt + vt] = soft_pack(s);
+    }
+  }
+}
+
 template <int NW, int MV, int NB, int KC, int NSTG, bool NTA>
 void launch_proj_bf16(const Launch& a, hipStream_t s) {
   const ProjPlan& p = a.plan;
@@ -210,8 +377,11 @@ void launch_proj_bf16(const Launch& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_proj_small(const Launch& a, hipStream_t s) {
-  if (a.plan.variant == PROJ_BF16_R32)
-    launch_proj_bf16<8, 4, 2, 64, 3, false>(a, s);
+  const ProjPlan& p = a.plan;
+  if (p.variant == PROJ_BF16_R32)
+    hipLaunchKernelGGL((k_proj_bf16_stream<kStreamWaves, kStreamBlocks>), dim3(p.grid), dim3(kStreamWaves * 64), 0,
+                       s, static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
+                       a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows);
   else
     launch_proj_bf16<8, 4, 4, 64, 3, false>(a, s);
   return hipGetLastError();

@@ -12,7 +12,7 @@ namespace rpd {
 // row r = p*K + l for compacted masked position p. A "vocab tile" is a
 // contiguous range of W_U rows; tile t covers [t*V/NVT, (t+1)*V/NVT).
 enum ProjVariant {
-  PROJ_BF16_R32 = 0,   // small row count: 32 rows per tile, 8 waves x 64 vocab
+  PROJ_BF16_R32 = 0,   // <= 32 rows: 4 independent waves x 64 vocab rows, W_U through wave-private LDS
   PROJ_BF16_R64 = 1,   // 64 rows per tile, 8 waves x 64 vocab
   PROJ_BF16_M32 = 2,   // up to 192 rows: 32x32 MFMA, 128 rows per tile, 8 waves x 64 vocab
   PROJ_F32 = 3,        // fp32 inputs: vector ALU, 16 rows x 64 vocab
@@ -21,6 +21,10 @@ enum ProjVariant {
 
 // tile of the large-row variant: vocabulary rows x projected rows
 constexpr int kBigTileVocab = 256, kBigTileRows = 256;
+// the <= 32-row streaming variant: waves per workgroup and 32-row W_U
+// blocks per wave (a workgroup covers 32 * kStreamWaves * kStreamBlocks
+// vocabulary rows)
+constexpr int kStreamWaves = 4, kStreamBlocks = 2;
 
 struct ProjPlan {
   ProjVariant variant;
@@ -45,6 +49,7 @@ struct Launch {
   // workspace pieces
   int32_t* n_masked;     // [1] device count (clamped to max_masked)
   int32_t* dev_status;   // [1] internal status word
+  int32_t* done;         // [1] completion counter of the fused reduction + commitment
   int32_t* rows;         // [max_masked] compacted b*L+i
   float4* partials;      // [K*max_masked][nvt]
   ProjPlan plan;
@@ -60,11 +65,14 @@ struct Launch {
 };
 
 // enqueue, in this order: compaction, projection, reduction + scoring,
-// commitment (the last three use a.plan and a.max_masked)
+// commitment (the last three use a.plan and a.max_masked). When
+// commit_fused(a), the reduction kernel's last workgroup runs the commitment
+// and launch_commit is not called.
 hipError_t launch_compact(const Launch& a, hipStream_t s);
 hipError_t launch_projection(const Launch& a, hipStream_t s);
 hipError_t launch_reduce_score(const Launch& a, hipStream_t s);
 hipError_t launch_commit(const Launch& a, hipStream_t s);
+bool commit_fused(const Launch& a);
 
 // the projection variants, dispatched by launch_projection on a.plan.variant
 hipError_t launch_proj_small(const Launch& a, hipStream_t s);   // PROJ_BF16_R32, PROJ_BF16_R64

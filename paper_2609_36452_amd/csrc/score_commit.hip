@@ -11,7 +11,7 @@ namespace {
 __global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ mask, int BL, int cap,
                                                    int32_t* __restrict__ rows, int32_t* __restrict__ n_out,
                                                    int32_t* __restrict__ dev_status,
-                                                   int32_t* __restrict__ user_status) {
+                                                   int32_t* __restrict__ user_status, int32_t* __restrict__ done) {
   __shared__ int wsum[16];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
   int carry = 0;
@@ -41,6 +41,7 @@ __global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ ma
     }
     *n_out = n;
     *dev_status = st;
+    *done = 0;   // completion counter of the fused reduction + commitment
     if (user_status) *user_status = st;
   }
 }
@@ -80,73 +81,75 @@ struct ScoreArgs {
 // and stability with one lane per layer.
 constexpr int kReduceWaves = 4;
 
-__global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4* __restrict__ partials,
-                                                                     const int32_t* __restrict__ rows,
-                                                                     const int32_t* __restrict__ n_ptr, int nvt,
-                                                                     ScoreArgs a) {
-  __shared__ int ly[64];
-  __shared__ float lc[64], lh[64];
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int p = blockIdx.x;
-  if (p >= *n_ptr) return;
-  const int pos = rows[p];
-  const int b = pos / a.L, i = pos - b * a.L;
+// Fixed-order merge of one row's nvt vocabulary-tile states by one wave:
+// lane folds tiles lane, lane+64, ... in tile order (loads batched four at a
+// time), then an xor butterfly combines the lanes. Every lane returns the
+// row's state.
+__device__ __forceinline__ Soft wave_merge_row(const float4* __restrict__ src, int nvt, int lane) {
   const float4 empty = soft_pack(soft_empty());
-  for (int l = wid; l < a.K; l += kReduceWaves) {
-    const float4* src = partials + ((long long)p * a.K + l) * nvt;
-    Soft s = soft_empty();
-    for (int t0 = lane; t0 < nvt; t0 += 64 * 4) {
-      float4 v[4];
+  Soft s = soft_empty();
+  for (int t0 = lane; t0 < nvt; t0 += 64 * 4) {
+    float4 v[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = (t0 + 64 * u < nvt) ? src[t0 + 64 * u] : empty;
+    for (int u = 0; u < 4; ++u) v[u] = (t0 + 64 * u < nvt) ? src[t0 + 64 * u] : empty;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) s = soft_merge(s, soft_unpack(v[u]));
-    }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) s = soft_merge(s, soft_shfl_xor(s, m));
-    if (lane == 0) {
-      const float h = fmaxf(logf(s.S) - s.T / s.S, 0.0f);
-      ly[l] = (s.idx == INT_MAX) ? -1 : s.idx;
-      lc[l] = 1.0f / s.S;
-      lh[l] = (s.S != s.S) ? s.S : h;   // keep NaN visible
-    }
+    for (int u = 0; u < 4; ++u) s = soft_merge(s, soft_unpack(v[u]));
   }
-  __syncthreads();
-  if (wid != 0) return;
-  const int my_y = lane < a.K ? ly[lane] : -1;
-  const float my_c = lane < a.K ? lc[lane] : 0.f;
-  const float my_h = lane < a.K ? lh[lane] : 0.f;
-  const int yK = ly[a.K - 1];
-  const float cK = lc[a.K - 1];
-  const float hK = lh[a.K - 1];
-  // Eq. 2: agreement suffix ending at the final layer
-  const unsigned long long dis = __ballot(lane < a.K && my_y != yK);
-  const int last_dis = dis ? 63 - __clzll(dis) : -1;
-  const int k_i = a.K - 1 - last_dis;
-  // Eq. 3: inside the suffix the final token is each layer's argmax, so its
-  // probability there is that layer's top probability
-  float pk = (lane >= a.K - k_i && lane < a.K) ? my_c : -INFINITY;
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) pk = fmaxf(pk, __shfl_xor(pk, m));
-  const float r_i = pk - cK;
-  const float s_i = stability_score(k_i, r_i, a.k_max, a.w);
-  const unsigned fl = route_flags(cK, s_i, a.theta_h, a.theta_c, a.theta_s);
-  const long long o = (long long)b * a.L + i;
-  if (lane == 0) {
-    a.token[o] = yK;
-    a.entropy[o] = hK;
-    a.confidence[o] = cK;
-    a.persistence[o] = k_i;
-    a.drop[o] = r_i;
-    a.stability[o] = s_i;
-    a.flags[o] = (uint8_t)fl;
+  for (int m = 32; m >= 1; m >>= 1) s = soft_merge(s, soft_shfl_xor(s, m));
+  return s;
+}
+
+// argmax (-1 if none), top probability 1/S and entropy ln S - T/S (Eq. 1) of
+// a merged state; NaN stays visible in the entropy
+__device__ __forceinline__ void state_stats(const Soft& s, int& y, float& c, float& h) {
+  const float e = fmaxf(logf(s.S) - s.T / s.S, 0.0f);
+  y = (s.idx == INT_MAX) ? -1 : s.idx;
+  c = 1.0f / s.S;
+  h = (s.S != s.S) ? s.S : e;
+}
+
+
+// Eq. 2-5 for one position from its per-layer argmax / top probability /
+// entropy (layer l at offset l * stride), evaluated sequentially from the
+// final layer down the agreement suffix. Inside the suffix the final token is
+// each layer's argmax, so its probability there is that layer's top
+// probability (Eq. 3). Same results as the wave-parallel form in
+// k_reduce_score (the maximum is exact in any order).
+struct Scored {
+  int y, k;
+  float c, h, r, s;
+  unsigned flags;
+};
+template <typename TY, typename TF>
+__device__ __forceinline__ Scored score_layers(const TY* y, const TF* c, const TF* h, long long stride,
+                                              const ScoreArgs& a) {
+  Scored o;
+  o.y = y[(long long)(a.K - 1) * stride];
+  o.c = c[(long long)(a.K - 1) * stride];
+  o.h = h[(long long)(a.K - 1) * stride];
+  int k_i = 1;
+  float pk = o.c;
+  for (int l = a.K - 2; l >= 0; --l) {
+    if (y[(long long)l * stride] != o.y) break;
+    ++k_i;
+    pk = fmaxf(pk, c[(long long)l * stride]);
   }
-  if (a.layer_argmax && lane < a.K) {
-    const long long ol = ((long long)lane * a.B + b) * a.L + i;
-    a.layer_argmax[ol] = my_y;
-    a.layer_conf[ol] = my_c;
-    a.layer_entropy[ol] = my_h;
-  }
+  o.k = k_i;
+  o.r = pk - o.c;
+  o.s = stability_score(k_i, o.r, a.k_max, a.w);
+  o.flags = route_flags(o.c, o.s, a.theta_h, a.theta_c, a.theta_s);
+  return o;
+}
+
+__device__ __forceinline__ void write_scored(const ScoreArgs& a, long long o, const Scored& sc) {
+  a.token[o] = sc.y;
+  a.entropy[o] = sc.h;
+  a.confidence[o] = sc.c;
+  a.persistence[o] = sc.k;
+  a.drop[o] = sc.r;
+  a.stability[o] = sc.s;
+  a.flags[o] = (uint8_t)sc.flags;
 }
 
 // Scoring from caller-supplied per-layer statistics, one thread per canvas
@@ -158,25 +161,8 @@ __global__ __launch_bounds__(256) void k_gate_score(const uint8_t* __restrict__ 
   const long long BL = (long long)a.B * a.L;
   const long long o = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (o >= BL || mask[o] == 0) return;
-  const int yK = l_y[(long long)(a.K - 1) * BL + o];
-  const float cK = l_c[(long long)(a.K - 1) * BL + o];
-  const float hK = l_h[(long long)(a.K - 1) * BL + o];
-  int k_i = 1;
-  float pk = cK;
-  for (int l = a.K - 2; l >= 0; --l) {
-    if (l_y[(long long)l * BL + o] != yK) break;
-    ++k_i;
-    pk = fmaxf(pk, l_c[(long long)l * BL + o]);
-  }
-  const float r_i = pk - cK;
-  const float s_i = stability_score(k_i, r_i, a.k_max, a.w);
-  a.token[o] = yK;
-  a.entropy[o] = hK;
-  a.confidence[o] = cK;
-  a.persistence[o] = k_i;
-  a.drop[o] = r_i;
-  a.stability[o] = s_i;
-  a.flags[o] = (uint8_t)route_flags(cK, s_i, a.theta_h, a.theta_c, a.theta_s);
+  const Scored sc = score_layers(l_y + o, l_c + o, l_h + o, BL, a);
+  write_scored(a, o, sc);
 }
 
 // --------------------------------------------------- commitment (Sec. 3.2) --
@@ -229,20 +215,44 @@ struct CommitArgs {
   int32_t* n_commit;
 };
 
-// One workgroup per sequence. N_i = entropy summed over earlier masked
-// non-candidates; a candidate is committed iff N_i <= beta, which is exactly
-// the left-to-right construction of the paper (every earlier candidate of an
-// accepted position is accepted, so the positions left out before it are the
-// non-candidates; a rejected candidate's sum only grows). E_i (reported) is
-// the entropy over earlier masked positions not committed. Without any
-// commit, the most confident of the first `window` masked positions is
-// committed (lowest index on ties; NaN confidences never win).
-__global__ __launch_bounds__(kCommitThreads) void k_commit(const uint8_t* __restrict__ mask, CommitArgs a) {
+// Where the commitment reads a masked position's scoring results: the
+// output arrays (k_commit), or arrays indexed by masked rank in LDS
+// (k_finish; ranks past `n` were not scored and count as non-candidates of
+// zero entropy).
+struct GlobalScores {
+  const uint8_t* flags;
+  const float* entropy;
+  const float* confidence;
+  __device__ unsigned flag(long long o, int) const { return flags[o]; }
+  __device__ float ent(long long o, int) const { return entropy[o]; }
+  __device__ float conf(long long o, int) const { return confidence[o]; }
+};
+struct RankScores {
+  const uint8_t* flags;
+  const float* entropy;
+  const float* confidence;
+  int n;
+  __device__ unsigned flag(long long, int r) const { return r < n ? flags[r] : 0u; }
+  __device__ float ent(long long, int r) const { return r < n ? entropy[r] : 0.f; }
+  __device__ float conf(long long, int r) const { return r < n ? confidence[r] : -INFINITY; }
+};
+
+// The commitment of sequence b by the whole workgroup. N_i = entropy summed
+// over earlier masked non-candidates; a candidate is committed iff
+// N_i <= beta, which is exactly the left-to-right construction of the paper
+// (every earlier candidate of an accepted position is accepted, so the
+// positions left out before it are the non-candidates; a rejected
+// candidate's sum only grows). E_i (reported) is the entropy over earlier
+// masked positions not committed. Without any commit, the most confident of
+// the first `window` masked positions is committed (lowest index on ties;
+// NaN confidences never win). Unmasked positions receive the sentinels.
+template <class Scores>
+__device__ __forceinline__ void commit_sequence(const uint8_t* __restrict__ mask, const CommitArgs& a, int b,
+                                                const Scores& sc) {
   __shared__ float shf[64];
   __shared__ int shi[64];
   __shared__ float red_c[16];
   __shared__ int red_i[16];
-  const int b = blockIdx.x;
   const long long base = (long long)b * a.L;
   float carryN = 0.f, carryE = 0.f;
   int carryM = 0, ncommit = 0;
@@ -251,26 +261,26 @@ __global__ __launch_bounds__(kCommitThreads) void k_commit(const uint8_t* __rest
   for (int c0 = 0; c0 < a.L; c0 += blockDim.x) {
     const int i = c0 + threadIdx.x;
     const bool in = i < a.L;
-    const bool masked = in && mask[base + i] != 0;
-    const unsigned fl = masked ? a.flags[base + i] : 0u;
-    const bool cand = (fl & kFlagCandidate) != 0;
-    const float H = masked ? a.entropy[base + i] : 0.f;
-    float totN, totE;
+    const long long o = base + i;
+    const bool masked = in && mask[o] != 0;
     int totM;
+    const int rank = carryM + block_exclusive_scan<int>(masked ? 1 : 0, shi, totM);
+    const unsigned fl = masked ? sc.flag(o, rank) : 0u;
+    const bool cand = (fl & kFlagCandidate) != 0;
+    const float H = masked ? sc.ent(o, rank) : 0.f;
+    float totN, totE;
     const float N_i = carryN + block_exclusive_scan<float>((masked && !cand) ? H : 0.f, shf, totN);
     const bool com = masked && cand && (N_i <= a.beta);
     const float E_i = carryE + block_exclusive_scan<float>((masked && !com) ? H : 0.f, shf, totE);
-    const int rank = carryM + block_exclusive_scan<int>(masked ? 1 : 0, shi, totM);
     int ncom_chunk;
     (void)block_exclusive_scan<int>(com ? 1 : 0, shi, ncom_chunk);
     if (in) {
-      const long long o = base + i;
       if (masked) {
         a.commit[o] = com ? 1 : 0;
         a.flags[o] = (uint8_t)(fl | (com ? kFlagCommitted : 0u));
         a.upstream_entropy[o] = E_i;
         if (rank < a.window) {
-          float cv = a.confidence[o];
+          float cv = sc.conf(o, rank);
           cv = (cv != cv) ? -INFINITY : cv;
           if (cv > best_c || (cv == best_c && i < best_i)) {
             best_c = cv;
@@ -330,6 +340,85 @@ __global__ __launch_bounds__(kCommitThreads) void k_commit(const uint8_t* __rest
   if (threadIdx.x == 0) a.n_commit[b] = ncommit;
 }
 
+// K3 alone: one workgroup per sequence, scoring results from the outputs
+__global__ __launch_bounds__(kCommitThreads) void k_commit(const uint8_t* __restrict__ mask, CommitArgs a) {
+  commit_sequence(mask, a, blockIdx.x, GlobalScores{a.flags, a.entropy, a.confidence});
+}
+
+// K2: one workgroup of four waves per masked position. Wave w merges the
+// vocab-tile states of layers w, w+4, ... (wave_merge_row); wave 0 then
+// evaluates persistence, drop and stability with one lane per layer. With
+// FUSE (a batch of one sequence), the last workgroup to finish, found with a
+// device-scope counter that the compaction zeroed, also runs the commitment
+// (K3), which saves its launch.
+template <bool FUSE>
+__global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4* __restrict__ partials,
+                                                                     const int32_t* __restrict__ rows,
+                                                                     const int32_t* __restrict__ n_ptr, int nvt,
+                                                                     ScoreArgs a, const uint8_t* __restrict__ mask,
+                                                                     CommitArgs ca, int32_t* __restrict__ done) {
+  __shared__ int ly[64];
+  __shared__ float lc[64], lh[64];
+  __shared__ int s_last;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int p = blockIdx.x;
+  const int n = *n_ptr;
+  if (!FUSE && p >= n) return;
+  if (p < n) {
+    const int pos = rows[p];
+    const int b = pos / a.L, i = pos - b * a.L;
+    for (int l = wid; l < a.K; l += kReduceWaves) {
+      const Soft s = wave_merge_row(partials + ((long long)p * a.K + l) * nvt, nvt, lane);
+      if (lane == 0) state_stats(s, ly[l], lc[l], lh[l]);
+    }
+    __syncthreads();
+    if (wid == 0) {
+      const int my_y = lane < a.K ? ly[lane] : -1;
+      const float my_c = lane < a.K ? lc[lane] : 0.f;
+      const float my_h = lane < a.K ? lh[lane] : 0.f;
+      const int yK = ly[a.K - 1];
+      const float cK = lc[a.K - 1];
+      const float hK = lh[a.K - 1];
+      // Eq. 2: agreement suffix ending at the final layer
+      const unsigned long long dis = __ballot(lane < a.K && my_y != yK);
+      const int last_dis = dis ? 63 - __clzll(dis) : -1;
+      const int k_i = a.K - 1 - last_dis;
+      // Eq. 3: inside the suffix the final token is each layer's argmax, so
+      // its probability there is that layer's top probability
+      float pk = (lane >= a.K - k_i && lane < a.K) ? my_c : -INFINITY;
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) pk = fmaxf(pk, __shfl_xor(pk, m));
+      const float r_i = pk - cK;
+      const float s_i = stability_score(k_i, r_i, a.k_max, a.w);
+      const unsigned fl = route_flags(cK, s_i, a.theta_h, a.theta_c, a.theta_s);
+      const long long o = (long long)b * a.L + i;
+      if (lane == 0) {
+        a.token[o] = yK;
+        a.entropy[o] = hK;
+        a.confidence[o] = cK;
+        a.persistence[o] = k_i;
+        a.drop[o] = r_i;
+        a.stability[o] = s_i;
+        a.flags[o] = (uint8_t)fl;
+      }
+      if (a.layer_argmax && lane < a.K) {
+        const long long ol = ((long long)lane * a.B + b) * a.L + i;
+        a.layer_argmax[ol] = my_y;
+        a.layer_conf[ol] = my_c;
+        a.layer_entropy[ol] = my_h;
+      }
+    }
+  }
+  if (!FUSE) return;
+  __threadfence();   // this workgroup's outputs, visible device-wide before it is counted
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = p < n ? (atomicAdd(done, 1) == n - 1) : (n == 0 && p == 0);
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();   // every other workgroup's outputs are visible from here on
+  commit_sequence(mask, ca, 0, GlobalScores{ca.flags, ca.entropy, ca.confidence});
+}
+
 ScoreArgs score_args(const Launch& a) {
   ScoreArgs s;
   s.K = a.K;
@@ -376,14 +465,20 @@ CommitArgs commit_args(const Launch& a) {
 
 hipError_t launch_compact(const Launch& a, hipStream_t s) {
   hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, a.mask, a.B * a.L, a.max_masked, a.rows, a.n_masked,
-                     a.dev_status, a.user_status);
+                     a.dev_status, a.user_status, a.done);
   return hipGetLastError();
 }
 
+bool commit_fused(const Launch& a) { return a.B == 1 && a.max_masked > 0; }
+
 hipError_t launch_reduce_score(const Launch& a, hipStream_t s) {
   if (a.max_masked <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_reduce_score, dim3(a.max_masked), dim3(64 * kReduceWaves), 0, s, a.partials, a.rows,
-                     a.n_masked, a.plan.nvt, score_args(a));
+  if (commit_fused(a))
+    hipLaunchKernelGGL(k_reduce_score<true>, dim3(a.max_masked), dim3(64 * kReduceWaves), 0, s, a.partials, a.rows,
+                       a.n_masked, a.plan.nvt, score_args(a), a.mask, commit_args(a), a.done);
+  else
+    hipLaunchKernelGGL(k_reduce_score<false>, dim3(a.max_masked), dim3(64 * kReduceWaves), 0, s, a.partials,
+                       a.rows, a.n_masked, a.plan.nvt, score_args(a), a.mask, commit_args(a), a.done);
   return hipGetLastError();
 }
 

@@ -41,9 +41,9 @@ def _a256(x):
 
 
 def test_workspace_size():
-    # late-decode LLaDA shape: header + row list + (32 rows x 256 tiles x 16 B)
+    # late-decode LLaDA shape: header + row list + (32 rows x 512 tiles of 256 vocabulary rows x 16 B)
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=8)
-    assert n == 256 + 1024 + _a256(32 * 256 * 16)
+    assert n == 256 + 1024 + _a256(32 * 512 * 16)
     # 10% masked: 104 rows x 247 tiles of 512 vocabulary rows
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=26)
     assert n == 256 + 1024 + _a256(104 * 247 * 16)
