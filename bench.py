@@ -29,15 +29,11 @@ RIDGE_ROWS = 315             # projected rows where the projection turns compute
 METRIC = "masked positions scored+committed/sec at LLaDA-8B shape; MFMA % / HBM GB/s"
 CSRC = os.path.join(ROOT, "paper_2609_36452_amd", "csrc")
 # the source files that define each projection variant's kernel
-VARIANT_SOURCES = {
-    "bf16_r32": ["rpd_device.h", "proj_stage.h", "proj_small.hip"],
-    "bf16_r64": ["rpd_device.h", "proj_stage.h", "proj_small.hip"],
-    "bf16_m32": ["rpd_device.h", "proj_stage.h", "proj_mid.hip"],
-    "bf16_big": ["rpd_device.h", "proj_big.hip"],
-    "f32": ["rpd_device.h", "proj_f32.hip"],
-}
-VARIANT_KERNEL = {"bf16_r32": "k_proj_bf16_stream", "bf16_r64": "k_proj_bf16", "bf16_m32": "k_proj_bf16_m32",
-                  "bf16_big": "k_proj_bf16_big", "f32": "k_proj_f32"}
+VARIANT_SOURCES = {v: ["rpd_device.h", "proj_stream.hip"] for v in
+                   ("bf16_s32", "bf16_s64", "bf16_s128", "bf16_s192", "bf16_s256")}
+VARIANT_SOURCES.update({"bf16_big": ["rpd_device.h", "proj_big.hip"], "f32": ["rpd_device.h", "proj_f32.hip"]})
+VARIANT_KERNEL = {v: "k_proj_bf16_stream" for v in ("bf16_s32", "bf16_s64", "bf16_s128", "bf16_s192", "bf16_s256")}
+VARIANT_KERNEL.update({"bf16_big": "k_proj_bf16_big", "f32": "k_proj_f32"})
 COPY_PROBE_BYTES = 1 << 30     # fp32 elements read (and as many written) by the copy probe
 
 

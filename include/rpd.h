@@ -195,11 +195,13 @@ rpd_status rpd_gate_commit(int32_t K, int32_t B, int32_t L, const uint8_t* mask,
 
 /* projection kernel variants (values of rpd_projection_variant) */
 enum {
-  RPD_PROJ_BF16_R32 = 0, /* bf16, at most 32 projected rows: HBM-bound W_U stream */
-  RPD_PROJ_BF16_R64 = 1, /* bf16, 33..64 rows */
-  RPD_PROJ_BF16_M32 = 2, /* bf16, 65..192 rows */
-  RPD_PROJ_F32 = 3,      /* fp32 inputs, any row count */
-  RPD_PROJ_BF16_BIG = 4  /* bf16, more than 192 rows: MFMA-bound 256 x 256 tiles */
+  RPD_PROJ_BF16_S32 = 0,  /* bf16, at most 32 projected rows: W_U streamed once from HBM */
+  RPD_PROJ_BF16_S64 = 1,  /* bf16, 33..64 rows, same kernel family */
+  RPD_PROJ_BF16_S128 = 2, /* bf16, 65..128 rows */
+  RPD_PROJ_F32 = 3,       /* fp32 inputs, any row count */
+  RPD_PROJ_BF16_BIG = 4,  /* bf16, more than 256 rows: MFMA-bound 256 x 256 tiles */
+  RPD_PROJ_BF16_S192 = 5, /* bf16, 129..192 rows */
+  RPD_PROJ_BF16_S256 = 6  /* bf16, 193..256 rows */
 };
 
 /*

@@ -18,19 +18,20 @@ ProjPlan plan_projection(int dtype, long long rows_cap, int V) {
     p.grid = p.nvt * p.nrt;
     return p;
   }
-  if (rows_cap <= 64) {
-    p.variant = rows_cap <= 32 ? PROJ_BF16_R32 : PROJ_BF16_R64;
-    p.rows_per_tile = rows_cap <= 32 ? 32 : 64;
-    p.vocab_cap = rows_cap <= 32 ? 32 * kStreamWaves * kStreamBlocks : 8 * 64;
-    // every CU streams an equal share of W_U: a multiple of 256 tiles
+  if (rows_cap <= 256) {
+    // HBM-bound: one row tile holding every projected row, so W_U is read
+    // once; a multiple of 256 equal vocabulary tiles, so every CU streams the
+    // same share
+    p.variant = rows_cap <= 32    ? PROJ_BF16_S32
+                : rows_cap <= 64  ? PROJ_BF16_S64
+                : rows_cap <= 128 ? PROJ_BF16_S128
+                : rows_cap <= 192 ? PROJ_BF16_S192
+                                  : PROJ_BF16_S256;
+    p.rows_per_tile = rows_cap <= 32 ? 32 : rows_cap <= 64 ? 64 : rows_cap <= 128 ? 128 : rows_cap <= 192 ? 192 : 256;
+    p.vocab_cap = kStreamTileVocab;
     int nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
     nvt = ((nvt + 255) / 256) * 256;
     p.nvt = nvt < V ? nvt : V;
-  } else if (rows_cap <= 192) {
-    p.variant = PROJ_BF16_M32;
-    p.rows_per_tile = 128;
-    p.vocab_cap = 8 * 64;
-    p.nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
   } else {
     p.variant = PROJ_BF16_BIG;
     p.rows_per_tile = kBigTileRows;
@@ -47,9 +48,11 @@ ProjPlan plan_projection(int dtype, long long rows_cap, int V) {
 hipError_t launch_projection(const Launch& a, hipStream_t s) {
   if (a.max_masked <= 0) return hipSuccess;
   switch (a.plan.variant) {
-    case PROJ_BF16_R32:
-    case PROJ_BF16_R64: return launch_proj_small(a, s);
-    case PROJ_BF16_M32: return launch_proj_mid(a, s);
+    case PROJ_BF16_S32:
+    case PROJ_BF16_S64:
+    case PROJ_BF16_S128:
+    case PROJ_BF16_S192:
+    case PROJ_BF16_S256: return launch_proj_stream(a, s);
     case PROJ_BF16_BIG: return launch_proj_big(a, s);
     case PROJ_F32: return launch_proj_f32(a, s);
   }

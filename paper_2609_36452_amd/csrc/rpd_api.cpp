@@ -46,7 +46,7 @@ size_t workspace_bytes_for(const rpd_problem* p, long long cap) {
   const long long rows = (long long)p->K * cap;
   size_t part = partial_bytes(rpd::plan_projection(p->dtype, rows, p->V), rows);
   if (p->max_masked < 0) {
-    for (long long r : {32LL, 64LL, 65LL, 192LL, 193LL}) {
+    for (long long r : {32LL, 33LL, 64LL, 65LL, 128LL, 129LL, 192LL, 193LL, 256LL, 257LL}) {
       const long long rr = r < rows ? r : rows;
       const size_t b = partial_bytes(rpd::plan_projection(p->dtype, rr, p->V), rr);
       if (b > part) part = b;

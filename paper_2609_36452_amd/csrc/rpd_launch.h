@@ -12,19 +12,19 @@ namespace rpd {
 // row r = p*K + l for compacted masked position p. A "vocab tile" is a
 // contiguous range of W_U rows; tile t covers [t*V/NVT, (t+1)*V/NVT).
 enum ProjVariant {
-  PROJ_BF16_R32 = 0,   // <= 32 rows: 4 independent waves x 64 vocab rows, W_U through wave-private LDS
-  PROJ_BF16_R64 = 1,   // 64 rows per tile, 8 waves x 64 vocab
-  PROJ_BF16_M32 = 2,   // up to 192 rows: 32x32 MFMA, 128 rows per tile, 8 waves x 64 vocab
-  PROJ_F32 = 3,        // fp32 inputs: vector ALU, 16 rows x 64 vocab
-  PROJ_BF16_BIG = 4,   // compute-bound: 256 x 256 tiles, both operands staged through LDS
+  PROJ_BF16_S32 = 0,    // <= 32 rows: W_U streamed through wave-private LDS, hidden rows shared
+  PROJ_BF16_S64 = 1,    // <= 64 rows, same kernel family
+  PROJ_BF16_S128 = 2,   // <= 128 rows
+  PROJ_F32 = 3,         // fp32 inputs: vector ALU, 16 rows x 64 vocab
+  PROJ_BF16_BIG = 4,    // > 256 rows, MFMA-bound: 256 x 256 tiles, both operands staged through LDS
+  PROJ_BF16_S192 = 5,   // <= 192 rows
+  PROJ_BF16_S256 = 6,   // <= 256 rows
 };
 
 // tile of the large-row variant: vocabulary rows x projected rows
 constexpr int kBigTileVocab = 256, kBigTileRows = 256;
-// the <= 32-row streaming variant: waves per workgroup and 32-row W_U
-// blocks per wave (a workgroup covers 32 * kStreamWaves * kStreamBlocks
-// vocabulary rows)
-constexpr int kStreamWaves = 4, kStreamBlocks = 2;
+// vocabulary rows of one workgroup of the streaming variants (all of them)
+constexpr int kStreamTileVocab = 256;
 
 struct ProjPlan {
   ProjVariant variant;
@@ -75,8 +75,7 @@ hipError_t launch_commit(const Launch& a, hipStream_t s);
 bool commit_fused(const Launch& a);
 
 // the projection variants, dispatched by launch_projection on a.plan.variant
-hipError_t launch_proj_small(const Launch& a, hipStream_t s);   // PROJ_BF16_R32, PROJ_BF16_R64
-hipError_t launch_proj_mid(const Launch& a, hipStream_t s);     // PROJ_BF16_M32
+hipError_t launch_proj_stream(const Launch& a, hipStream_t s);  // PROJ_BF16_S32 .. PROJ_BF16_S256
 hipError_t launch_proj_big(const Launch& a, hipStream_t s);     // PROJ_BF16_BIG
 hipError_t launch_proj_f32(const Launch& a, hipStream_t s);     // PROJ_F32
 

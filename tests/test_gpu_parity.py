@@ -3,8 +3,9 @@
 Small and mid-size cases are compared element by element (every masked
 position, every layer); they span several vocabulary and row tiles, ragged
 vocabulary sizes and hidden sizes that are not multiples of the 64-wide
-k-chunk, and every projection variant (<= 32, <= 64, <= 192 and more
-projected rows, with row tiles split across XCDs). Full-size LLaDA-8B / Dream-7B shapes are
+k-chunk, and every projection variant (the streaming family at <= 32, 64,
+128, 192 and 256 projected rows, and the MFMA tile above, with row tiles
+split across XCDs). Full-size LLaDA-8B / Dream-7B shapes are
 compared on sampled positions that the oracle computes one by one, plus the
 prefix-sum identity of the commitment on the GPU's own outputs."""
 import math
@@ -59,11 +60,12 @@ def test_tiny_f32_calibrated(seed, pname):
 
 BF16_CASES = [
     # name (the projection variant the case runs, then what it exercises), overrides, seed;
-    # rows = K * masked
-    ("bf16_r32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
-    ("bf16_r64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10, masked_frac=None), 12),
-    ("bf16_m32_one_tile", dict(B=1, L=40, K=4, d=4104, V=2500, n_masked=20, masked_frac=None), 15),
-    ("bf16_m32_two_tiles", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=20, masked_frac=None), 16),
+    # rows = K * masked. Hidden sizes: whole 64-wide chunks, odd chunk counts, ragged tails.
+    ("bf16_s32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
+    ("bf16_s64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10, masked_frac=None), 12),
+    ("bf16_s128_long_d", dict(B=1, L=40, K=4, d=4104, V=2500, n_masked=20, masked_frac=None), 15),
+    ("bf16_s192_two_seqs", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=20, masked_frac=None), 16),
+    ("bf16_s256_odd_chunks", dict(B=1, L=80, K=3, d=200, V=6007, n_masked=80, masked_frac=None), 17),
     ("bf16_big_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
     ("bf16_big_row_split", dict(B=4, L=600, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
 ]
