@@ -6,6 +6,57 @@
 namespace rpd {
 namespace {
 
+// The masked-position compaction (K0) folded into the projection's
+// prologue, for small canvases: every workgroup scans the mask itself (while
+// its first W_U loads are in flight) and keeps the first `need` positions;
+// workgroup 0 also publishes the list, the count and the status for the
+// kernels that follow, exactly as k_compact does.
+struct CompactArgs {
+  const uint8_t* mask;
+  int BL, cap;
+  int32_t* rows;
+  int32_t* n;
+  int32_t* dev_status;
+  int32_t* user_status;
+  int32_t* done;
+};
+
+template <int NW>
+__device__ int compact_in_workgroup(const CompactArgs& ca, int* s_pos, int need, int* s_wave) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const bool publish = blockIdx.x == 0;
+  int carry = 0;
+  for (int base = 0; base < ca.BL; base += NW * 64) {
+    const int i = base + threadIdx.x;
+    const bool f = i < ca.BL && ca.mask[i] != 0;
+    const unsigned long long bal = __ballot(f);
+    const int before = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) s_wave[wid] = __popcll(bal);
+    __syncthreads();
+    int off = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const int c = s_wave[w];
+      off += (w < wid) ? c : 0;
+      tot += c;
+    }
+    const int rank = carry + off + before;
+    if (f && rank < need) s_pos[rank] = i;
+    if (f && publish && rank < ca.cap) ca.rows[rank] = i;
+    carry += tot;
+    __syncthreads();
+  }
+  const int n = carry < ca.cap ? carry : ca.cap;
+  if (publish && threadIdx.x == 0) {
+    const int st = carry > ca.cap ? 1 : 0;
+    *ca.n = n;
+    *ca.dev_status = st;
+    if (ca.user_status) *ca.user_status = st;
+    *ca.done = 0;   // completion counter of the fused reduction + commitment
+  }
+  return n;
+}
+
 // A workgroup of NW waves owns 32*MV*NW consecutive W_U rows (one
 // vocabulary tile) and all TR = 32*NB projected rows, over the full hidden
 // dimension, in 64-wide k-chunks.
@@ -33,11 +84,13 @@ namespace {
 // Measured at the LLaDA-8B shape (d = 4096, V = 126464): 156 us at 32 rows
 // (83% of 8 TB/s), 159 us at 64, 180 us at 128, 211 us at 192, 246 us at
 // 256; the 256 x 256 MFMA tile needs 298 us at 256 rows.
-template <int NW, int MV, int NB>
+//
+// FC: the workgroup compacts the mask itself (compact_in_workgroup).
+template <int NW, int MV, int NB, bool FC>
 __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
-    int nvt, int nrt, int split_rows) {
+    int nvt, int nrt, int split_rows, CompactArgs ca) {
   constexpr int TR = 32 * NB, WR = 32 * MV, KC = 64, NT = NW * 64;
   constexpr int NLD = WR / 8;          // W_U load instructions per wave per chunk
   constexpr int XLD = TR * 8 / NT;     // hidden-row pieces per thread per chunk
@@ -46,12 +99,12 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
   __shared__ __attribute__((aligned(16))) uint16_t wl[NW][WR][KC];
   __shared__ __attribute__((aligned(16))) uint16_t xl[2][TR][KC];
   __shared__ float4 red[NW][TR];
+  __shared__ int s_pos[FC ? TR : 1];
+  __shared__ int s_wave[NW];
 
-  int rt, vt;
-  if (!map_job(blockIdx.x, nvt, nrt, split_rows, rt, vt)) return;
-  const int R = *n_ptr * K;
-  const int r0 = rt * TR;
-  if (r0 >= R) return;
+  int rt = 0, vt = 0;
+  const bool has_job = map_job(blockIdx.x, nvt, nrt, split_rows, rt, vt);
+  if (!has_job && !(FC && blockIdx.x == 0)) return;   // workgroup 0 always publishes the compaction
   const int vb = (int)((long long)vt * V / nvt);
   const int ve = (int)((long long)(vt + 1) * V / nvt);
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -69,6 +122,28 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
     wa[u] = (long long)min(vw + row, ve - 1) * d + wpiece[u] * 8;
   }
   const int srow = lane >> 3, spc = (lane & 7) * 8;
+  u32x4 ld[D][NLD];
+  u32x4 xr[D][XLD];
+  const int nchf = d / KC;
+  // W_U loads of the first two chunks go out before anything waits
+  if (has_job && nchf > 0) {
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+#pragma unroll
+      for (int u = 0; u < NLD; ++u)
+        ld[j][u] = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>(w_u + wa[u] + (long long)min(j, nchf - 1) * KC));
+  }
+  int R;
+  if (FC) {
+    // one row tile (r0 = 0): rows 0 .. TR-1 need positions 0 .. TR-1 at most
+    R = compact_in_workgroup<NW>(ca, s_pos, TR, s_wave) * K;
+    if (!has_job) return;
+  } else {
+    R = *n_ptr * K;
+  }
+  const int r0 = rt * TR;
+  if (r0 >= R) return;
   // hidden rows: piece q = tid + NT*u is row q >> 3, LDS piece q & 7. Rows
   // past the last projected row re-read row r0 (their results are dropped).
   long long xa[XLD];
@@ -81,7 +156,7 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
     xpiece[u] = (q & 7) ^ ((row >> 1) & 7);
     const int r = r0 + row < R ? r0 + row : r0;
     const int p = r / K, l = r - p * K;
-    const int pos = rows[p];
+    const int pos = FC ? s_pos[p] : rows[p];
     const int b = pos / L, i = pos - b * L;
     xa[u] = (((long long)l * B + b) * L + i) * (long long)d + xpiece[u] * 8;
   }
@@ -96,17 +171,18 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[mv][nb][q] = 0.f;
-  u32x4 ld[D][NLD];
-  u32x4 xr[D][XLD];
-  const int nchf = d / KC;
-
+#define RPD_XLOAD(slot, chunk)                                                                           \
+  do {                                                                                                   \
+    const long long k0_ = (long long)(chunk) * KC;                                                       \
+    _Pragma("unroll") for (int u_ = 0; u_ < XLD; ++u_)                                                  \
+      xr[slot][u_] = *reinterpret_cast<const u32x4*>(hidden + xa[u_] + k0_);                             \
+  } while (0)
 #define RPD_SLOAD(slot, chunk)                                                                           \
   do {                                                                                                   \
     const long long k0_ = (long long)(chunk) * KC;                                                       \
     _Pragma("unroll") for (int u_ = 0; u_ < NLD; ++u_)                                                  \
       ld[slot][u_] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(w_u + wa[u_] + k0_));     \
-    _Pragma("unroll") for (int u_ = 0; u_ < XLD; ++u_)                                                  \
-      xr[slot][u_] = *reinterpret_cast<const u32x4*>(hidden + xa[u_] + k0_);                             \
+    RPD_XLOAD(slot, chunk);                                                                              \
   } while (0)
   // the MFMAs of one staged chunk (W_U in the wave's buffer, hidden rows in stage XS)
 #define RPD_SMMA(XS)                                                                                     \
@@ -140,8 +216,8 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
   } while (0)
 
   if (nchf > 0) {
-    RPD_SLOAD(0, 0);
-    RPD_SLOAD(1, min(1, nchf - 1));
+    RPD_XLOAD(0, 0);
+    RPD_XLOAD(1, min(1, nchf - 1));
     int c = 0;
     for (; c + 2 <= nchf; c += 2) {
       RPD_SCHUNK(c, 0, 0);
@@ -169,6 +245,7 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
 #undef RPD_SCHUNK
 #undef RPD_SMMA
 #undef RPD_SLOAD
+#undef RPD_XLOAD
 
   // epilogue: softmax state of the wave's vocabulary rows per projected row,
   // then a fixed-order merge over the waves
@@ -208,12 +285,25 @@ template <int NW, int MV, int NB>
 void launch_stream(const Launch& a, hipStream_t s) {
   static_assert(32 * MV * NW == kStreamTileVocab, "every streaming variant covers the same vocabulary tile");
   const ProjPlan& p = a.plan;
-  hipLaunchKernelGGL((k_proj_bf16_stream<NW, MV, NB>), dim3(p.grid), dim3(NW * 64), 0, s,
-                     static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
-                     a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows);
+  const CompactArgs ca{a.mask, a.B * a.L, a.max_masked, a.rows, a.n_masked, a.dev_status, a.user_status, a.done};
+  if (a.fused_compact)
+    hipLaunchKernelGGL((k_proj_bf16_stream<NW, MV, NB, true>), dim3(p.grid), dim3(NW * 64), 0, s,
+                       static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
+                       a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows, ca);
+  else
+    hipLaunchKernelGGL((k_proj_bf16_stream<NW, MV, NB, false>), dim3(p.grid), dim3(NW * 64), 0, s,
+                       static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
+                       a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows, ca);
 }
 
 }  // namespace
+
+bool compact_fused(const Launch& a) {
+  const ProjVariant v = a.plan.variant;
+  const bool streaming = v == PROJ_BF16_S32 || v == PROJ_BF16_S64 || v == PROJ_BF16_S128 || v == PROJ_BF16_S192 ||
+                         v == PROJ_BF16_S256;
+  return streaming && a.plan.nrt == 1 && a.max_masked > 0 && (long long)a.B * a.L <= kFusedCompactMax;
+}
 
 hipError_t launch_proj_stream(const Launch& a, hipStream_t s) {
   switch (a.plan.variant) {

@@ -174,8 +174,15 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
     if (k < n_events && events[k]) return hipEventRecord(static_cast<hipEvent_t>(events[k]), s);
     return hipSuccess;
   };
+  // with a known bound the plan comes first, and small canvases are
+  // compacted inside the projection kernel
+  a.fused_compact = false;
+  if (p->max_masked >= 0) {
+    a.plan = rpd::plan_projection(p->dtype, (long long)p->K * a.max_masked, p->V);
+    a.fused_compact = rpd::compact_fused(a);
+  }
   hipError_t e = mark(0);
-  if (e == hipSuccess) e = rpd::launch_compact(a, s);
+  if (e == hipSuccess && !a.fused_compact) e = rpd::launch_compact(a, s);
   if (e != hipSuccess) return fail(RPD_ERR_HIP, "compaction: %s", hipGetErrorString(e));
   if (p->max_masked < 0) {
     int32_t n = 0;
@@ -183,8 +190,8 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return fail(RPD_ERR_HIP, "reading the masked count: %s", hipGetErrorString(e));
     a.max_masked = n;
+    a.plan = rpd::plan_projection(p->dtype, (long long)p->K * a.max_masked, p->V);
   }
-  a.plan = rpd::plan_projection(p->dtype, (long long)p->K * a.max_masked, p->V);
   if ((e = mark(1)) == hipSuccess && (e = rpd::launch_projection(a, s)) == hipSuccess && (e = mark(2)) == hipSuccess &&
       (e = rpd::launch_reduce_score(a, s)) == hipSuccess && (e = mark(3)) == hipSuccess &&
       (rpd::commit_fused(a) || (e = rpd::launch_commit(a, s)) == hipSuccess))

@@ -25,6 +25,8 @@ enum ProjVariant {
 constexpr int kBigTileVocab = 256, kBigTileRows = 256;
 // vocabulary rows of one workgroup of the streaming variants (all of them)
 constexpr int kStreamTileVocab = 256;
+// largest canvas (B * L) whose compaction the streaming projection does itself
+constexpr int kFusedCompactMax = 2048;
 
 struct ProjPlan {
   ProjVariant variant;
@@ -50,6 +52,7 @@ struct Launch {
   int32_t* n_masked;     // [1] device count (clamped to max_masked)
   int32_t* dev_status;   // [1] internal status word
   int32_t* done;         // [1] completion counter of the fused reduction + commitment
+  bool fused_compact;    // the projection kernel does the compaction (no launch_compact)
   int32_t* rows;         // [max_masked] compacted b*L+i
   float4* partials;      // [K*max_masked][nvt]
   ProjPlan plan;
@@ -73,6 +76,9 @@ hipError_t launch_projection(const Launch& a, hipStream_t s);
 hipError_t launch_reduce_score(const Launch& a, hipStream_t s);
 hipError_t launch_commit(const Launch& a, hipStream_t s);
 bool commit_fused(const Launch& a);
+// the projection does the compaction itself (needs a.plan and a.max_masked
+// >= 0): the call then launches no compaction kernel
+bool compact_fused(const Launch& a);
 
 // the projection variants, dispatched by launch_projection on a.plan.variant
 hipError_t launch_proj_stream(const Launch& a, hipStream_t s);  // PROJ_BF16_S32 .. PROJ_BF16_S256

@@ -82,18 +82,18 @@ struct ScoreArgs {
 constexpr int kReduceWaves = 4;
 
 // Fixed-order merge of one row's nvt vocabulary-tile states by one wave:
-// lane folds tiles lane, lane+64, ... in tile order (loads batched four at a
-// time), then an xor butterfly combines the lanes. Every lane returns the
-// row's state.
+// lane folds tiles lane, lane+64, ... in tile order (loads batched eight at
+// a time: one round trip for up to 512 tiles), then an xor butterfly
+// combines the lanes. Every lane returns the row's state.
 __device__ __forceinline__ Soft wave_merge_row(const float4* __restrict__ src, int nvt, int lane) {
   const float4 empty = soft_pack(soft_empty());
   Soft s = soft_empty();
-  for (int t0 = lane; t0 < nvt; t0 += 64 * 4) {
-    float4 v[4];
+  for (int t0 = lane; t0 < nvt; t0 += 64 * 8) {
+    float4 v[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = (t0 + 64 * u < nvt) ? src[t0 + 64 * u] : empty;
+    for (int u = 0; u < 8; ++u) v[u] = (t0 + 64 * u < nvt) ? src[t0 + 64 * u] : empty;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) s = soft_merge(s, soft_unpack(v[u]));
+    for (int u = 0; u < 8; ++u) s = soft_merge(s, soft_unpack(v[u]));
   }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) s = soft_merge(s, soft_shfl_xor(s, m));
@@ -169,34 +169,53 @@ __global__ __launch_bounds__(256) void k_gate_score(const uint8_t* __restrict__ 
 
 constexpr int kCommitThreads = 1024;
 
-// exclusive prefix sum over the workgroup in thread order (fixed tree order);
-// `total` receives the sum of all values
-template <typename T>
-__device__ __forceinline__ T block_exclusive_scan(T v, T* sh, T& total) {
+// two exclusive prefix sums over the workgroup in thread order (a fixed
+// tree order: wave scans, then a scan of the wave totals); va / vb are
+// replaced by their prefixes, tota / totb receive the sums
+template <typename TA, typename TB>
+__device__ __forceinline__ void block_exclusive_scan2(TA& va, TB& vb, TA* sha, TB* shb, TA& tota, TB& totb) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  T x = v;
+  TA xa = va;
+  TB xb = vb;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    const T y = __shfl_up(x, o);
-    if (lane >= o) x = x + y;
+    const TA ya = __shfl_up(xa, o);
+    const TB yb = __shfl_up(xb, o);
+    if (lane >= o) {
+      xa = xa + ya;
+      xb = xb + yb;
+    }
   }
-  if (lane == 63) sh[wid] = x;
+  if (lane == 63) {
+    sha[wid] = xa;
+    shb[wid] = xb;
+  }
   __syncthreads();
   if (wid == 0) {
-    T s = (lane < nw) ? sh[lane] : T(0);
+    TA sa = (lane < nw) ? sha[lane] : TA(0);
+    TB sb = (lane < nw) ? shb[lane] : TB(0);
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-      const T y = __shfl_up(s, o);
-      if (lane >= o) s = s + y;
+      const TA ya = __shfl_up(sa, o);
+      const TB yb = __shfl_up(sb, o);
+      if (lane >= o) {
+        sa = sa + ya;
+        sb = sb + yb;
+      }
     }
-    if (lane < nw) sh[32 + lane] = s;   // inclusive over waves
+    if (lane < nw) {
+      sha[32 + lane] = sa;
+      shb[32 + lane] = sb;
+    }
   }
   __syncthreads();
-  const T wave_before = (wid == 0) ? T(0) : sh[32 + wid - 1];
-  total = sh[32 + nw - 1];
-  const T res = wave_before + x - v;
+  const TA wa = (wid == 0) ? TA(0) : sha[32 + wid - 1];
+  const TB wb = (wid == 0) ? TB(0) : shb[32 + wid - 1];
+  tota = sha[32 + nw - 1];
+  totb = shb[32 + nw - 1];
+  va = wa + xa - va;
+  vb = wb + xb - vb;
   __syncthreads();
-  return res;
 }
 
 struct CommitArgs {
@@ -215,26 +234,15 @@ struct CommitArgs {
   int32_t* n_commit;
 };
 
-// Where the commitment reads a masked position's scoring results: the
-// output arrays (k_commit), or arrays indexed by masked rank in LDS
-// (k_finish; ranks past `n` were not scored and count as non-candidates of
-// zero entropy).
+// Where the commitment reads a masked position's scoring results (the
+// output arrays, written by the scoring).
 struct GlobalScores {
   const uint8_t* flags;
   const float* entropy;
   const float* confidence;
-  __device__ unsigned flag(long long o, int) const { return flags[o]; }
-  __device__ float ent(long long o, int) const { return entropy[o]; }
-  __device__ float conf(long long o, int) const { return confidence[o]; }
-};
-struct RankScores {
-  const uint8_t* flags;
-  const float* entropy;
-  const float* confidence;
-  int n;
-  __device__ unsigned flag(long long, int r) const { return r < n ? flags[r] : 0u; }
-  __device__ float ent(long long, int r) const { return r < n ? entropy[r] : 0.f; }
-  __device__ float conf(long long, int r) const { return r < n ? confidence[r] : -INFINITY; }
+  __device__ unsigned flag(long long o) const { return flags[o]; }
+  __device__ float ent(long long o) const { return entropy[o]; }
+  __device__ float conf(long long o) const { return confidence[o]; }
 };
 
 // The commitment of sequence b by the whole workgroup. N_i = entropy summed
@@ -249,8 +257,8 @@ struct RankScores {
 template <class Scores>
 __device__ __forceinline__ void commit_sequence(const uint8_t* __restrict__ mask, const CommitArgs& a, int b,
                                                 const Scores& sc) {
-  __shared__ float shf[64];
-  __shared__ int shi[64];
+  __shared__ float shf[64], shf2[64];
+  __shared__ int shi[64], shi2[64];
   __shared__ float red_c[16];
   __shared__ int red_i[16];
   const long long base = (long long)b * a.L;
@@ -262,25 +270,31 @@ __device__ __forceinline__ void commit_sequence(const uint8_t* __restrict__ mask
     const int i = c0 + threadIdx.x;
     const bool in = i < a.L;
     const long long o = base + i;
+    // loads issued together (entries of unmasked positions are read and ignored)
     const bool masked = in && mask[o] != 0;
-    int totM;
-    const int rank = carryM + block_exclusive_scan<int>(masked ? 1 : 0, shi, totM);
-    const unsigned fl = masked ? sc.flag(o, rank) : 0u;
+    const unsigned fl_in = in ? sc.flag(o) : 0u;
+    const float H_in = in ? sc.ent(o) : 0.f;
+    const unsigned fl = masked ? fl_in : 0u;
     const bool cand = (fl & kFlagCandidate) != 0;
-    const float H = masked ? sc.ent(o, rank) : 0.f;
-    float totN, totE;
-    const float N_i = carryN + block_exclusive_scan<float>((masked && !cand) ? H : 0.f, shf, totN);
+    const float H = masked ? H_in : 0.f;
+    // masked rank and N_i in one pass, then E_i and the commit count
+    int rank = masked ? 1 : 0, totM;
+    float N_i = (masked && !cand) ? H : 0.f, totN;
+    block_exclusive_scan2<int, float>(rank, N_i, shi, shf, totM, totN);
+    rank += carryM;
+    N_i += carryN;
     const bool com = masked && cand && (N_i <= a.beta);
-    const float E_i = carryE + block_exclusive_scan<float>((masked && !com) ? H : 0.f, shf, totE);
-    int ncom_chunk;
-    (void)block_exclusive_scan<int>(com ? 1 : 0, shi, ncom_chunk);
+    float E_i = (masked && !com) ? H : 0.f, totE;
+    int ncom_before = com ? 1 : 0, ncom_chunk;
+    block_exclusive_scan2<float, int>(E_i, ncom_before, shf2, shi2, totE, ncom_chunk);
+    E_i += carryE;
     if (in) {
       if (masked) {
         a.commit[o] = com ? 1 : 0;
         a.flags[o] = (uint8_t)(fl | (com ? kFlagCommitted : 0u));
         a.upstream_entropy[o] = E_i;
         if (rank < a.window) {
-          float cv = sc.conf(o, rank);
+          float cv = sc.conf(o);
           cv = (cv != cv) ? -INFINITY : cv;
           if (cv > best_c || (cv == best_c && i < best_i)) {
             best_c = cv;
