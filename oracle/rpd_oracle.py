@@ -18,7 +18,10 @@ Every function follows a passage of the paper (He, Liu, Xiong, Zhang,
 * candidate set -- Eq. (5), Section 3.1;
 * sequential cumulative-entropy commitment and the progress fallback --
   Section 3.2 (definitions of ``E_i`` and ``A_t``), hyperparameters in
-  Table 4 (Appendix A.6).
+  Table 4 (Appendix A.6);
+* the RPD-block commitment -- Section 3.2 "Variants" and Appendix A.6
+  "RPD-block": the candidates of the active 32-position block, no budget,
+  fallback to the block's most confident masked position.
 
 Readings where the paper is silent (stated once here, used throughout):
 the supplied hidden states are already normalised (the projection is a plain
@@ -28,6 +31,10 @@ layer K-1 the final one; ``p^(l)(y_i)`` in the drop is the probability of the
 final-layer token; sequences of a batch are independent; "the first W masked
 positions" are the first W entries of the masked list in canvas order; the
 fallback ignores NaN confidences and picks the lowest index among equals.
+For RPD-block: blocks are consecutive runs of ``block`` canvas positions
+starting at position 0 of each sequence; the active block is the first one
+that still holds a masked position; ``E_i`` is still reported, as the
+entropy over earlier masked positions outside the commitment set.
 
 Arithmetic is float64 on the exact values of the bf16 / fp32 inputs.
 """
@@ -55,6 +62,7 @@ class Params:
     k_max: int = 6           # cap on persistence
     beta: float = 4.0        # cumulative entropy budget, nats
     window: int = 32         # fallback window W
+    block: int = 0           # 0: full RPD; > 0: RPD-block with blocks of this many positions
 
 
 LLADA = Params(theta_s=3.5, w=15.0)
@@ -228,6 +236,41 @@ def commit_scan(H: np.ndarray, cand: np.ndarray, c: np.ndarray, p: Params) -> di
     return {"commit": commit, "E": E, "fallback": fb}
 
 
+def commit_block(idx: np.ndarray, H: np.ndarray, cand: np.ndarray, c: np.ndarray, block: int) -> dict:
+    """RPD-block for one sequence (Section 3.2 "Variants"; Appendix A.6
+    "RPD-block"), on its masked positions in canvas order at canvas indices
+    ``idx``. The active block is the first run of ``block`` canvas positions
+    (runs start at 0) that holds a masked position; every candidate inside it
+    is committed and no entropy budget applies. If none is, the single most
+    confident masked position of the active block is committed. ``E`` reports
+    the entropy over earlier masked positions outside the commitment set
+    (before the fallback), as in commit_scan."""
+    n = len(H)
+    commit = np.zeros(n, bool)
+    E = np.zeros(n, np.float64)
+    fb = -1
+    if n == 0:
+        return {"commit": commit, "E": E, "fallback": fb}
+    lo = (int(idx[0]) // block) * block
+    active = (idx >= lo) & (idx < lo + block)
+    for q in range(n):
+        commit[q] = bool(cand[q] and active[q])
+    acc = 0.0
+    for q in range(n):
+        E[q] = acc
+        if not commit[q]:
+            acc = acc + H[q]
+    if not commit.any():
+        best = -np.inf
+        for q in range(n):
+            if active[q] and not np.isnan(c[q]) and (fb < 0 or c[q] > best):
+                best, fb = c[q], q
+        if fb < 0:   # every confidence in the block is NaN: the first masked position
+            fb = 0
+        commit[fb] = True
+    return {"commit": commit, "E": E, "fallback": fb}
+
+
 def commit_closed_form(H: np.ndarray, cand: np.ndarray, p: Params) -> dict:
     """Equivalent closed form of the budget test: with
     ``N_i = sum of H_j over earlier masked non-candidates``, the selected set
@@ -290,9 +333,13 @@ def select(mask: np.ndarray, layer: dict, p: Params, positions: list[tuple[int, 
             o["drop"][b, i] = r_i
             o["stability"][b, i] = s_i
             o["flags"][b, i] = (FLAG_CANDIDATE * (high or stab)) | (FLAG_HIGH_CONF * high) | (FLAG_STABLE * stab)
-        sc = commit_scan(H, cand, c, p)
-        cf = commit_closed_form(H, cand, p)
-        if not np.isnan(H).any():
+        if p.block > 0:
+            sc = commit_block(masked, H, cand, c, p.block)
+            cf = {"N": np.zeros(n)}
+        else:
+            sc = commit_scan(H, cand, c, p)
+            cf = commit_closed_form(H, cand, p)
+        if p.block == 0 and not np.isnan(H).any():
             pre = sc["commit"].copy()
             if sc["fallback"] >= 0:
                 pre[sc["fallback"]] = False

@@ -384,3 +384,87 @@ def test_calibrated_workload_populates_band():
         c = o["confidence"][w.mask == 1]
         band += int(((c >= 0.6) & (c < 0.9)).sum())
     assert band >= 20
+
+
+# ----------------------------------------------------------- RPD-block ----
+# Section 3.2 "Variants" and Appendix A.6 "RPD-block": candidate selection
+# inside the active 32-position block, no budget, fallback to the block's
+# most confident masked position.
+
+def test_block_hand_cases():
+    H = np.array([0.5, 2.0, 0.1, 0.3])
+    c = np.array([0.7, 0.95, 0.92, 0.8])
+    idx = np.array([1, 2, 5, 6])
+    # candidates at canvas 2 (active block [0, 4)) and 5 (next block): only 2 is committed
+    r = O.commit_block(idx, H, np.array([False, True, True, False]), c, 4)
+    assert r["commit"].tolist() == [False, True, False, False] and r["fallback"] == -1
+    # E_i: entropy of earlier masked positions outside the commitment set
+    assert r["E"].tolist() == [0.0, 0.5, 0.5, 0.6]
+    # no candidate in the active block: the most confident masked position of [0, 4) (canvas 2),
+    # not the globally most confident one
+    r = O.commit_block(idx, H, np.array([False, False, True, True]), np.array([0.7, 0.8, 0.99, 0.97]), 4)
+    assert r["commit"].tolist() == [False, True, False, False] and r["fallback"] == 1
+    # the first block without masked positions is skipped: active block [8, 16)
+    r = O.commit_block(np.array([9, 12, 17]), np.array([1.0, 1.0, 1.0]), np.array([False, True, True]),
+                       np.array([0.5, 0.5, 0.5]), 8)
+    assert r["commit"].tolist() == [False, True, False]
+    # ties: lowest index; NaN never wins
+    r = O.commit_block(np.array([0, 1, 2]), np.zeros(3), np.zeros(3, bool), np.array([np.nan, 0.4, 0.4]), 4)
+    assert r["fallback"] == 1
+    r = O.commit_block(np.array([0, 1]), np.zeros(2), np.zeros(2, bool), np.array([np.nan, np.nan]), 4)
+    assert r["fallback"] == 0
+
+
+def _random_sequence(rng, L):
+    idx = np.sort(rng.choice(L, size=rng.integers(1, L + 1), replace=False))
+    n = len(idx)
+    return idx, rng.exponential(1.0, n), rng.random(n) < 0.4, rng.uniform(0.2, 1.0, n)
+
+
+def test_block_of_one_commits_exactly_the_first_masked_position():
+    rng = np.random.default_rng(31)
+    for _ in range(200):
+        idx, H, cand, c = _random_sequence(rng, 40)
+        r = O.commit_block(idx, H, cand, c, 1)
+        assert r["commit"].tolist() == [True] + [False] * (len(idx) - 1)
+
+
+def test_block_covering_the_canvas_is_full_rpd_without_budget():
+    # one block over the whole canvas: every candidate is committed, else the most confident masked
+    # position -- the full rule with beta = inf and a fallback window covering the canvas
+    rng = np.random.default_rng(32)
+    for _ in range(200):
+        L = 40
+        idx, H, cand, c = _random_sequence(rng, L)
+        rb = O.commit_block(idx, H, cand, c, L)
+        rf = O.commit_scan(H, cand, c, O.Params(beta=math.inf, window=L))
+        assert np.array_equal(rb["commit"], rf["commit"]) and rb["fallback"] == rf["fallback"]
+        assert np.array_equal(rb["E"], rf["E"])
+
+
+def test_block_commits_never_leave_the_active_block():
+    rng = np.random.default_rng(33)
+    for _ in range(200):
+        idx, H, cand, c = _random_sequence(rng, 100)
+        blk = int(rng.integers(1, 40))
+        r = O.commit_block(idx, H, cand, c, blk)
+        lo = idx[0] // blk * blk
+        assert r["commit"].any()
+        assert ((idx[r["commit"]] >= lo) & (idx[r["commit"]] < lo + blk)).all()
+        inside = (idx >= lo) & (idx < lo + blk)
+        if (cand & inside).any():
+            assert np.array_equal(r["commit"], cand & inside)
+
+
+def test_block_mode_through_select():
+    # the whole rule on a tiny workload: per sequence, commits lie in the first block holding a masked
+    # position, and the flags agree with the commit mask
+    w = make_workload("tiny", 3)
+    P = O.Params(theta_s=2.0, w=1.0, block=8)
+    o = O.score_commit(w.hidden, w.w_u, w.mask, w.cfg.dtype, P)
+    for b in range(w.mask.shape[0]):
+        m = np.nonzero(w.mask[b])[0]
+        lo = m[0] // 8 * 8
+        com = np.nonzero(o["commit"][b])[0]
+        assert len(com) >= 1 and ((com >= lo) & (com < lo + 8)).all()
+        assert np.array_equal(o["commit"][b] != 0, (o["flags"][b] & O.FLAG_COMMITTED) != 0)
