@@ -13,6 +13,7 @@ layers), the regime where streaming the 1.04 GB unembedding bounds the step.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -129,7 +130,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="llada_late")
     ap.add_argument("--seed", type=int, default=1)
-    ap.add_argument("--rule", default="strict", choices=["strict", "llada", "dream"])
+    ap.add_argument("--rule", default="strict", choices=["strict", "llada", "dream", "llada_block"],
+                    help="commit rule: strict agreement (default), the paper's LLaDA / Dream settings, or "
+                         "RPD-block with the LLaDA settings and blocks of 32")
     ap.add_argument("--beta", type=float, default=1.0)
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -159,6 +162,8 @@ def main() -> int:
         P = rpd.Params.strict(cfg.K, args.beta)
     elif args.rule == "llada":
         P = rpd.Params.llada()
+    elif args.rule == "llada_block":
+        P = dataclasses.replace(rpd.Params.llada(), block=32)
     else:
         P = rpd.Params.dream()
     dev = torch.device("cuda:0")
@@ -236,8 +241,10 @@ def main() -> int:
         "dtype": cfg.dtype,
         "data": "synthetic (seeded random W_U ~ N(0,1/d) and hidden states of the model shape)",
         "config": {"workload": f"{cfg.name}: d={cfg.d} V={cfg.V} B={cfg.B} L={cfg.L} K={cfg.K} "
-                               f"masked={n} ({R} projected rows), rule={args.rule} beta={P.beta}",
-                   "masked_positions": n, "projected_rows": R, "seed": args.seed},
+                               f"masked={n} ({R} projected rows), rule={args.rule} beta={P.beta}"
+                               + (f" block={P.block}" if P.block else ""),
+                   "masked_positions": n, "projected_rows": R, "seed": args.seed,
+                   "commit_rule": "rpd_block" if P.block else "rpd"},
         "iterations_per_s": round(1e3 / ms_step, 1),
         "roofline": roof,
     }

@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define RPD_ABI_VERSION 1
+#define RPD_ABI_VERSION 2
 
 /* element type of `hidden` and `w_u` (both must have the same type) */
 enum { RPD_DTYPE_BF16 = 0, RPD_DTYPE_F32 = 1 };
@@ -99,7 +99,19 @@ typedef struct rpd_problem {
  * Hyperparameters (Table 4, Appendix A.6; LLaDA: theta_s 3.5, w 15; Dream:
  * theta_s 2.5, w 20; both theta_h 0.9, theta_c 0.6, K_max 6, beta 4 nats,
  * W 32). Requirements: 0 <= theta_c <= theta_h, w >= 0, k_max >= 1,
- * beta >= 0 (may be +inf), window >= 1, flags == 0 (reserved); no NaN.
+ * beta >= 0 (may be +inf), window >= 1, flags == 0 (reserved), block >= 0;
+ * no NaN.
+ *
+ * block selects the commitment rule. 0: full RPD (Section 3.2), the
+ * cumulative-entropy budget beta over the whole canvas with the fallback
+ * over the first `window` masked positions. > 0: RPD-block (Section 3.2
+ * "Variants", Appendix A.6 "RPD-block"; the paper uses 32): the canvas of
+ * each sequence is cut into runs of `block` positions starting at 0, the
+ * active block is the first run holding a masked position, every candidate
+ * (Eq. 5) inside it is committed with no budget (beta and window are then
+ * unused), and without one its most confident masked position is. The
+ * reported upstream entropy is then the entropy over earlier masked
+ * positions outside the commitment set.
  */
 typedef struct rpd_params {
   float theta_h;   /* high-confidence threshold (bypasses stability), Eq. 5 */
@@ -110,6 +122,7 @@ typedef struct rpd_params {
   float beta;      /* cumulative entropy budget in nats, Section 3.2 */
   int32_t window;  /* fallback window W, Section 3.2 */
   uint32_t flags;  /* reserved, must be 0 */
+  int32_t block;   /* 0: full RPD; > 0: RPD-block with blocks of this many positions */
 } rpd_params;
 
 /*

@@ -40,7 +40,7 @@ class RpdProblem(ctypes.Structure):
 class RpdParams(ctypes.Structure):
     _fields_ = [("theta_h", ctypes.c_float), ("theta_c", ctypes.c_float), ("theta_s", ctypes.c_float),
                 ("w", ctypes.c_float), ("k_max", ctypes.c_int32), ("beta", ctypes.c_float),
-                ("window", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+                ("window", ctypes.c_int32), ("flags", ctypes.c_uint32), ("block", ctypes.c_int32)]
 
 
 _OUT_FIELDS = ["commit", "token", "entropy", "confidence", "persistence", "drop", "stability", "flags",
@@ -61,6 +61,7 @@ class Params:
     k_max: int = 6
     beta: float = 4.0
     window: int = 32
+    block: int = 0     # 0: full RPD; > 0: RPD-block with blocks of this many positions
 
     @staticmethod
     def llada() -> "Params":
@@ -78,7 +79,7 @@ class Params:
 
     def to_c(self) -> RpdParams:
         return RpdParams(self.theta_h, self.theta_c, self.theta_s, self.w, int(self.k_max), self.beta,
-                         int(self.window), 0)
+                         int(self.window), 0, int(self.block))
 
 
 class RpdError(RuntimeError):

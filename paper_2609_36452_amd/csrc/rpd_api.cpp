@@ -67,6 +67,7 @@ rpd_status check_params(const rpd_params* q) {
   if (std::isnan(q->beta) || q->beta < 0.f) return fail(RPD_ERR_BAD_PARAM, "beta must be >= 0 (got %g)", q->beta);
   if (q->window < 1) return fail(RPD_ERR_BAD_PARAM, "window must be >= 1 (got %d)", q->window);
   if (q->flags != 0) return fail(RPD_ERR_BAD_PARAM, "flags is reserved and must be 0");
+  if (q->block < 0) return fail(RPD_ERR_BAD_PARAM, "block must be >= 0 (got %d)", q->block);
   return RPD_OK;
 }
 
@@ -89,6 +90,7 @@ void fill_common(rpd::Launch& a, const rpd_params* q, const rpd_outputs* o) {
   a.beta = q->beta;
   a.k_max = q->k_max;
   a.window = q->window;
+  a.block = q->block;
   a.commit = o->commit;
   a.token = o->token;
   a.entropy = o->entropy;

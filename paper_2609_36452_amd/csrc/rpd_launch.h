@@ -59,6 +59,7 @@ struct Launch {
   // params
   float theta_h, theta_c, theta_s, w, beta;
   int k_max, window;
+  int block;             // 0: full RPD; > 0: RPD-block
   // outputs
   uint8_t* commit; int32_t* token; float* entropy; float* confidence;
   int32_t* persistence; float* drop; float* stability; uint8_t* flags;

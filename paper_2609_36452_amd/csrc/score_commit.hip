@@ -222,6 +222,7 @@ struct CommitArgs {
   int B, L;
   float beta;
   int window;
+  int block;   // 0: full RPD; > 0: RPD-block with blocks of this many positions
   uint8_t* commit;
   int32_t* token;
   float* entropy;
@@ -262,6 +263,26 @@ __device__ __forceinline__ void commit_sequence(const uint8_t* __restrict__ mask
   __shared__ float red_c[16];
   __shared__ int red_i[16];
   const long long base = (long long)b * a.L;
+  // RPD-block: the active block is the run of a.block positions holding the
+  // first masked position of the sequence
+  int blo = 0, bhi = 0;
+  if (a.block > 0) {
+    int first = INT_MAX;
+    for (int c0 = 0; c0 < a.L && first == INT_MAX; c0 += blockDim.x) {
+      const int i = c0 + threadIdx.x;
+      int f = (i < a.L && mask[base + i] != 0) ? i : INT_MAX;
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) f = min(f, __shfl_xor(f, m));
+      if ((threadIdx.x & 63) == 0) shi[threadIdx.x >> 6] = f;
+      __syncthreads();
+      for (int w = 0; w < (int)(blockDim.x >> 6); ++w) first = min(first, shi[w]);
+      __syncthreads();
+    }
+    if (first != INT_MAX) {
+      blo = first / a.block * a.block;
+      bhi = blo + a.block;
+    }
+  }
   float carryN = 0.f, carryE = 0.f;
   int carryM = 0, ncommit = 0;
   float best_c = -INFINITY;
@@ -283,7 +304,8 @@ __device__ __forceinline__ void commit_sequence(const uint8_t* __restrict__ mask
     block_exclusive_scan2<int, float>(rank, N_i, shi, shf, totM, totN);
     rank += carryM;
     N_i += carryN;
-    const bool com = masked && cand && (N_i <= a.beta);
+    const bool in_block = i >= blo && i < bhi;
+    const bool com = masked && cand && (a.block > 0 ? in_block : (N_i <= a.beta));
     float E_i = (masked && !com) ? H : 0.f, totE;
     int ncom_before = com ? 1 : 0, ncom_chunk;
     block_exclusive_scan2<float, int>(E_i, ncom_before, shf2, shi2, totE, ncom_chunk);
@@ -293,7 +315,7 @@ __device__ __forceinline__ void commit_sequence(const uint8_t* __restrict__ mask
         a.commit[o] = com ? 1 : 0;
         a.flags[o] = (uint8_t)(fl | (com ? kFlagCommitted : 0u));
         a.upstream_entropy[o] = E_i;
-        if (rank < a.window) {
+        if (a.block > 0 ? in_block : (rank < a.window)) {
           float cv = sc.conf(o);
           cv = (cv != cv) ? -INFINITY : cv;
           if (cv > best_c || (cv == best_c && i < best_i)) {
@@ -343,7 +365,7 @@ __device__ __forceinline__ void commit_sequence(const uint8_t* __restrict__ mask
           bc = red_c[w];
           bi = red_i[w];
         }
-      if (bi != INT_MAX) {   // the window always holds a masked position here
+      if (bi != INT_MAX) {   // the window (or the active block) always holds a masked position here
         const long long o = base + bi;
         a.commit[o] = 1;
         a.flags[o] = (uint8_t)(a.flags[o] | kFlagCommitted | kFlagFallback);
@@ -462,6 +484,7 @@ CommitArgs commit_args(const Launch& a) {
   c.L = a.L;
   c.beta = a.beta;
   c.window = a.window;
+  c.block = a.block;
   c.commit = a.commit;
   c.token = a.token;
   c.entropy = a.entropy;

@@ -149,7 +149,9 @@ def compare(g: dict, o: dict, mask: np.ndarray, P, d: int, layer: bool = True) -
         slack = slack + np.concatenate([[0.0], np.cumsum(np.where(cand_excused[b, idx],
                                                                   np.nan_to_num(o["entropy"][b, idx]), 0.0))[:-1]])
         N = o["budget_prefix"][b, idx]
-        budget_tie = np.abs(N - P.beta) <= slack
+        block = getattr(P, "block", 0)
+        # RPD-block has no budget: no commit decision sits near beta
+        budget_tie = np.zeros(idx.size, bool) if block > 0 else np.abs(N - P.beta) <= slack
         gcm = g["commit"][b, idx] != 0
         ocm = o["commit"][b, idx] != 0
         gfb = (g["flags"][b, idx] & F_FALLBACK) > 0
@@ -157,8 +159,12 @@ def compare(g: dict, o: dict, mask: np.ndarray, P, d: int, layer: bool = True) -
         excusable_seq = bool(cand_excused[b, idx].any() or budget_tie[ocand].any())
         rep.checked["commit"] += idx.size
         if gfb.any() or ofb.any():
-            # fallback on either side: compare the chosen position
-            win = idx[:P.window]
+            # fallback on either side: compare the chosen position (RPD-block: within the active block)
+            if block > 0:
+                lo = idx[0] // block * block
+                win = idx[(idx >= lo) & (idx < lo + block)]
+            else:
+                win = idx[:P.window]
             cw = np.nan_to_num(o["confidence"][b, win], nan=-np.inf)
             top2 = np.sort(cw)[-2:] if cw.size >= 2 else cw
             near = cw.size >= 2 and (top2[-1] - top2[0]) <= 2 * CONF_TOL

@@ -30,8 +30,13 @@ def test_exports_every_declared_symbol():
         assert hasattr(L, n), n
 
 
+def test_params_struct_layout():
+    # rpd_params of include/rpd.h: eight 4-byte fields, then block
+    assert ctypes.sizeof(rpd.RpdParams) == 36 and rpd.RpdParams.block.offset == 32
+
+
 def test_version_and_status_strings():
-    assert rpd.abi_version() == 1
+    assert rpd.abi_version() == 2
     assert rpd.status_string(0) == "ok"
     assert rpd.status_string(4) == "workspace too small"
 
@@ -87,7 +92,7 @@ def _prob(**kw):
 
 
 def _params(**kw):
-    p = dict(theta_h=0.9, theta_c=0.6, theta_s=3.5, w=15.0, k_max=6, beta=4.0, window=32, flags=0)
+    p = dict(theta_h=0.9, theta_c=0.6, theta_s=3.5, w=15.0, k_max=6, beta=4.0, window=32, flags=0, block=0)
     p.update(kw)
     return rpd.RpdParams(**p)
 
@@ -105,7 +110,7 @@ def test_problem_validation(kw, status):
 
 @pytest.mark.parametrize("kw", [dict(theta_c=0.95), dict(theta_c=-0.1), dict(w=-1.0), dict(k_max=0),
                                 dict(beta=-1.0), dict(beta=math.nan), dict(window=0), dict(flags=1),
-                                dict(theta_h=math.nan), dict(theta_s=math.inf)])
+                                dict(theta_h=math.nan), dict(theta_s=math.inf), dict(block=-1)])
 def test_param_validation(kw):
     s, msg = _call(_prob(), _params(**kw), _fake_outputs())
     assert s == 3, msg

@@ -84,6 +84,28 @@ def test_bf16_variants(name, ov, seed, sharp):
         _check(w, P)
 
 
+# ------------------------------------------------------------ RPD-block --
+
+@pytest.mark.parametrize("block", [32, 1, 7, 48])
+def test_rpd_block_commitment(block):
+    # Section 3.2 "Variants" / Appendix A.6 "RPD-block": candidates of the active block, no budget
+    w = make_workload(CONFIGS["llada_late"].with_(name="blk", B=3, L=48, K=4, d=256, V=3001, n_masked=None,
+                                                  masked_frac=0.6, sharp=("calibrated",), unstable_frac=0.3), 41)
+    for P in (O.Params(theta_s=3.5, w=15.0, block=block), O.Params(theta_s=2.5, w=20.0, block=block, beta=0.0)):
+        g, o, _ = _check(w, P)
+        for b in range(w.cfg.B):
+            m = np.nonzero(w.mask[b])[0]
+            lo = m[0] // block * block
+            com = np.nonzero(g["commit"][b])[0]
+            assert len(com) >= 1 and ((com >= lo) & (com < lo + block)).all()
+
+
+def test_rpd_block_at_late_decode_shape():
+    # the headline shape with the paper's block size
+    w = make_workload("llada_late", 3)
+    _check(w, O.Params(theta_s=3.5, w=15.0, block=32))
+
+
 # ------------------------------------------------------------- edge cases --
 
 def _small_bf16(seed=5, **ov):
@@ -164,7 +186,8 @@ def test_deterministic_bitwise():
         np.testing.assert_array_equal(a[k], b[k], err_msg=k)
 
 
-def test_gate_commit_matches_oracle_selection():
+@pytest.mark.parametrize("block", [0, 32, 5])
+def test_gate_commit_matches_oracle_selection(block):
     rng = np.random.default_rng(3)
     K, B, L = 6, 3, 200
     mask = (rng.random((B, L)) < 0.7).astype(np.uint8)
@@ -174,7 +197,7 @@ def test_gate_commit_matches_oracle_selection():
         y[l][keep] = y[K - 1][keep]
     conf = rng.uniform(0.3, 1.0, size=(K, B, L)).astype(np.float32)
     ent = rng.exponential(0.7, size=(K, B, L)).astype(np.float32)
-    P = O.Params(theta_s=4.5, w=10.0, beta=3.0)
+    P = O.Params(theta_s=4.5, w=10.0, beta=3.0, block=block)
     pos = O.masked_positions(mask)
     layer = {"argmax": np.array([y[:, b, i] for b, i in pos]).reshape(-1, K),
              "conf": np.array([conf[:, b, i] for b, i in pos], np.float64).reshape(-1, K),
@@ -198,7 +221,7 @@ def test_gate_commit_matches_oracle_selection():
     seq_ok = ~near.any(1)
     for b in np.nonzero(seq_ok)[0]:
         Nb = o["budget_prefix"][b][m[b]]
-        if np.any(np.abs(Nb - P.beta) < 1e-4):
+        if block == 0 and np.any(np.abs(Nb - P.beta) < 1e-4):
             continue
         np.testing.assert_array_equal(g["commit"][b], o["commit"][b])
         np.testing.assert_array_equal(g["flags"][b], o["flags"][b])
