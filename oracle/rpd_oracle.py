@@ -11,6 +11,10 @@ Every function follows a passage of the paper (He, Liu, Xiong, Zhang,
 * projection of hidden states through the unembedding ("logit lens") --
   Section 2.2 and Appendix A.2 "Intermediate-layer readout", Appendix A.6
   "Layerwise projection";
+* the model's final normalization applied to intermediate states before the
+  output head, with the final layer's native (already normalized) state
+  used as is -- Appendix A.2 "Intermediate-layer readout", Appendix A.6
+  "Layerwise projection";
 * entropy ``H(p) = -sum_v p(v) log p(v)`` in nats -- Eq. (1), Section 2.1;
 * prediction persistence ``K_i`` -- Eq. (2), Section 2.2 and Appendix A.2;
 * confidence drop ``r_i`` -- Eq. (3), Section 2.2 and Appendix A.2;
@@ -37,6 +41,12 @@ that still holds a masked position; ``E_i`` is still reported, as the
 entropy over earlier masked positions outside the commitment set.
 
 Arithmetic is float64 on the exact values of the bf16 / fp32 inputs.
+The final normalization is RMS normalization with a gain vector g,
+``g * x / sqrt(mean(x^2) + eps)``, evaluated in float64 and rounded (round
+to nearest, ties to even) to the input type, since the model's
+normalization hands the output head a state of that type. An optional
+logit scale (an inverse temperature, 1 by default, the paper's reading)
+multiplies every logit before the softmax statistics.
 """
 from __future__ import annotations
 
@@ -63,6 +73,7 @@ class Params:
     beta: float = 4.0        # cumulative entropy budget, nats
     window: int = 32         # fallback window W
     block: int = 0           # 0: full RPD; > 0: RPD-block with blocks of this many positions
+    logit_scale: float = 1.0  # multiplies every logit before the softmax statistics (1 / temperature)
 
 
 LLADA = Params(theta_s=3.5, w=15.0)
@@ -86,6 +97,27 @@ def to_f64(a: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "f32":
         return np.asarray(a, dtype=np.float32).astype(np.float64)
     raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def round_to_bf16(v: np.ndarray) -> np.ndarray:
+    """float64 -> the nearest bfloat16 value (8 significant bits, ties to
+    even), returned as float64. Normal range: v = m 2^e with 0.5 <= |m| < 1,
+    kept to m rounded at 2^-8; below 2^-126 the grid is 2^-133."""
+    v = np.asarray(v, np.float64)
+    m, e = np.frexp(v)
+    normal = np.round(m * 256.0) * np.exp2(e.astype(np.float64) - 8.0)   # np.round: ties to even
+    sub = np.round(v * 2.0 ** 133) * 2.0 ** -133
+    return np.where(np.abs(v) < 2.0 ** -126, sub, normal)
+
+
+def final_norm(x: np.ndarray, g: np.ndarray, eps: float, dtype: str) -> np.ndarray:
+    """The model's final normalization applied to a state before the output
+    head (Appendix A.2 "Intermediate-layer readout"): RMS normalization
+    ``g * x / sqrt(mean(x^2) + eps)`` in float64, rounded to the input type.
+    ``x`` and ``g`` are exact float64 values of the inputs."""
+    x = np.asarray(x, np.float64)
+    n = np.asarray(g, np.float64) * x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
+    return round_to_bf16(n) if dtype == "bf16" else n.astype(np.float32).astype(np.float64)
 
 
 # ------------------------------------------------- distribution statistics --
@@ -122,13 +154,17 @@ def _top2_gap(z: np.ndarray, y: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
 
 def project_layer_stats(hidden: np.ndarray, w_u: np.ndarray, dtype: str,
                         positions: list[tuple[int, int]], w_rows_per_chunk: int = 8192,
-                        max_bytes: int = 1 << 30) -> dict:
+                        max_bytes: int = 1 << 30, norm: tuple | None = None,
+                        logit_scale: float = 1.0) -> dict:
     """Per-layer statistics at the given canvas positions.
 
     For each position (b, i) and each supplied layer l the logits are
-    ``z = W_U x`` with ``x = hidden[l][b][i]`` (Section 2.2: intermediate
-    states read out through the output head; Appendix A.6: only masked
-    positions are projected). Returns arrays shaped [npos][K]:
+    ``z = logit_scale * W_U x`` with ``x = hidden[l][b][i]`` (Section 2.2:
+    intermediate states read out through the output head; Appendix A.6: only
+    masked positions are projected). With ``norm = (g, eps, norm_final)`` the
+    states of layers 0 .. K-2 (and of layer K-1 too if ``norm_final``) first
+    go through final_norm, ``g`` given like the hidden states (bf16 bit
+    patterns or fp32). Returns arrays shaped [npos][K]:
     ``argmax, conf, entropy`` of each layer's distribution, ``p_final`` =
     probability at layer l of the final layer's argmax token, and two
     diagnostics for classifying near-ties: ``gap`` (top-1 minus top-2 logit)
@@ -145,10 +181,16 @@ def project_layer_stats(hidden: np.ndarray, w_u: np.ndarray, dtype: str,
         blk = positions[p0:p0 + per_block]
         nb = len(blk)
         x = np.stack([to_f64(hidden[l, b, i], dtype) for (b, i) in blk for l in range(K)])  # [nb*K][d]
+        if norm is not None:
+            g, eps, norm_final = norm
+            gf = to_f64(g, dtype)
+            for a in range(nb):
+                for l in range(K if norm_final else K - 1):
+                    x[a * K + l] = final_norm(x[a * K + l], gf, eps, dtype)
         z = np.empty((nb * K, V), np.float64)
         for v0 in range(0, V, w_rows_per_chunk):
             wc = to_f64(w_u[v0:v0 + w_rows_per_chunk], dtype)
-            z[:, v0:v0 + wc.shape[0]] = x @ wc.T
+            z[:, v0:v0 + wc.shape[0]] = logit_scale * (x @ wc.T)
         z = z.reshape(nb, K, V)
         st = distribution_stats(z)
         y_final = st["argmax"][:, K - 1]
@@ -158,7 +200,7 @@ def project_layer_stats(hidden: np.ndarray, w_u: np.ndarray, dtype: str,
             for l in range(K):
                 xr = np.abs(x[a * K + l])
                 rows = to_f64(w_u[[st["argmax"][a, l], second[a, l]]], dtype)
-                absb[a, l] = (np.abs(rows) @ xr).max()
+                absb[a, l] = abs(logit_scale) * (np.abs(rows) @ xr).max()
         sl = slice(p0, p0 + nb)
         out["argmax"][sl] = st["argmax"]
         out["conf"][sl] = st["conf"]
@@ -361,10 +403,11 @@ def masked_positions(mask: np.ndarray) -> list[tuple[int, int]]:
     return [(b, int(i)) for b in range(B) for i in np.nonzero(mask[b])[0]]
 
 
-def layer_stats_masked(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str):
+def layer_stats_masked(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str,
+                       norm: tuple | None = None, logit_scale: float = 1.0):
     """Per-layer statistics of every masked position (canvas order)."""
     pos = masked_positions(mask)
-    return pos, project_layer_stats(hidden, w_u, dtype, pos)
+    return pos, project_layer_stats(hidden, w_u, dtype, pos, norm=norm, logit_scale=logit_scale)
 
 
 def assemble(mask: np.ndarray, pos: list, layer: dict, p: Params) -> dict:
@@ -381,9 +424,12 @@ def assemble(mask: np.ndarray, pos: list, layer: dict, p: Params) -> dict:
     return o
 
 
-def score_commit(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params) -> dict:
+def score_commit(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params,
+                 norm: tuple | None = None) -> dict:
     """The whole commit step for one decoding iteration: project every masked
     position at every supplied layer, score, select candidates and commit.
-    ``hidden[K][B][L][d]``, ``w_u[V][d]``, ``mask[B][L]`` (1 = masked)."""
-    pos, layer = layer_stats_masked(hidden, w_u, mask, dtype)
+    ``hidden[K][B][L][d]``, ``w_u[V][d]``, ``mask[B][L]`` (1 = masked);
+    ``norm = (g, eps, norm_final)`` normalizes the states first
+    (project_layer_stats)."""
+    pos, layer = layer_stats_masked(hidden, w_u, mask, dtype, norm=norm, logit_scale=p.logit_scale)
     return assemble(mask, pos, layer, p)

@@ -468,3 +468,74 @@ def test_block_mode_through_select():
         com = np.nonzero(o["commit"][b])[0]
         assert len(com) >= 1 and ((com >= lo) & (com < lo + 8)).all()
         assert np.array_equal(o["commit"][b] != 0, (o["flags"][b] & O.FLAG_COMMITTED) != 0)
+
+
+# ------------------------------------------- final normalization, scale ----
+# Appendix A.2 "Intermediate-layer readout" / A.6 "Layerwise projection": the
+# model's final normalization and output head are applied to intermediate
+# states; the final layer's native state is used as is.
+
+def test_round_to_bf16_against_torch_and_hand_values():
+    import torch
+    # ties to even at 8 significant bits
+    assert O.round_to_bf16(np.array([1 + 2 ** -8]))[0] == 1.0
+    assert O.round_to_bf16(np.array([1 + 3 * 2 ** -8]))[0] == 1 + 2 ** -6
+    assert O.round_to_bf16(np.array([-(1 + 3 * 2 ** -8)]))[0] == -(1 + 2 ** -6)
+    assert O.round_to_bf16(np.array([1 + 2 ** -8 + 2 ** -30]))[0] == 1 + 2 ** -7
+    # fp32-representable values: torch's round-to-nearest-even conversion
+    rng = np.random.default_rng(40)
+    v = (rng.standard_normal(20000) * np.exp2(rng.integers(-20, 20, 20000))).astype(np.float32)
+    ref = torch.from_numpy(v).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.round_to_bf16(v.astype(np.float64)), ref)
+
+
+def test_final_norm_is_torch_rms_norm():
+    import torch
+    rng = np.random.default_rng(41)
+    x = rng.standard_normal((5, 96)) * 3.0
+    g = rng.uniform(0.5, 2.0, 96)
+    for eps in (0.0, 1e-5, 1e-2):
+        ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (96,), torch.from_numpy(g), eps).numpy()
+        got = O.final_norm(x, g, eps, "f32")
+        np.testing.assert_allclose(got, ref, rtol=2 ** -23, atol=0)
+        np.testing.assert_array_equal(O.final_norm(x, g, eps, "bf16"), O.round_to_bf16(ref))
+
+
+def test_final_norm_is_scale_invariant():
+    # without eps, scaling a state by a power of two leaves its normalization unchanged exactly
+    rng = np.random.default_rng(42)
+    x = rng.standard_normal((3, 64))
+    g = rng.uniform(0.5, 2.0, 64)
+    for c in (2.0 ** -5, 2.0 ** 7):
+        np.testing.assert_array_equal(O.final_norm(c * x, g, 0.0, "bf16"), O.final_norm(x, g, 0.0, "bf16"))
+
+
+def test_norm_leaves_the_final_layer_native():
+    w = make_workload("tiny", 5)
+    pos = O.masked_positions(w.mask)[:6]
+    g = np.full(w.cfg.d, 1.5, np.float32)
+    plain = O.project_layer_stats(w.hidden, w.w_u, w.cfg.dtype, pos)
+    normed = O.project_layer_stats(w.hidden, w.w_u, w.cfg.dtype, pos, norm=(g, 1e-6, False))
+    both = O.project_layer_stats(w.hidden, w.w_u, w.cfg.dtype, pos, norm=(g, 1e-6, True))
+    K = w.cfg.K
+    for k in ("argmax", "conf", "entropy"):
+        np.testing.assert_array_equal(normed[k][:, K - 1], plain[k][:, K - 1])
+        np.testing.assert_array_equal(both[k][:, :K - 1], normed[k][:, :K - 1])
+    assert not np.allclose(normed["entropy"][:, :K - 1], plain["entropy"][:, :K - 1])
+
+
+def test_logit_scale_is_a_softmax_temperature():
+    w = make_workload("tiny", 6)
+    pos = O.masked_positions(w.mask)[:4]
+    base = O.project_layer_stats(w.hidden, w.w_u, w.cfg.dtype, pos)
+    for s in (0.5, 3.0):
+        st = O.project_layer_stats(w.hidden, w.w_u, w.cfg.dtype, pos, logit_scale=s)
+        np.testing.assert_array_equal(st["argmax"], base["argmax"])   # the order of the logits is kept
+        x = O.to_f64(w.hidden[:, pos[0][0], pos[0][1]], w.cfg.dtype)
+        z = s * (x @ O.to_f64(w.w_u, w.cfg.dtype).T)
+        p = scipy.special.softmax(z, axis=-1)
+        np.testing.assert_allclose(st["conf"][0], p.max(-1), rtol=1e-12)
+        np.testing.assert_allclose(st["entropy"][0], scipy.stats.entropy(p, axis=-1), rtol=1e-9, atol=1e-12)
+    # a sharper distribution has lower entropy
+    sharp = O.project_layer_stats(w.hidden, w.w_u, w.cfg.dtype, pos, logit_scale=4.0)
+    assert (sharp["entropy"] <= base["entropy"] + 1e-12).all()
