@@ -136,6 +136,8 @@ def main() -> int:
     ap.add_argument("--beta", type=float, default=1.0)
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--norm", action="store_true",
+                    help="pass a normalization gain: layers 0..K-2 go through the final normalization first")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain copy kernel of known size (for scaling HBM byte counters)")
     args = ap.parse_args()
@@ -174,7 +176,14 @@ def main() -> int:
         hidden = torch.from_numpy(w.hidden).to(dev)
         w_u = torch.from_numpy(w.w_u).to(dev)
     mask = torch.from_numpy(w.mask).to(dev)
-    call = rpd.ScoreCommit(hidden, w_u, mask, P, max_masked=w.n_masked)
+    norm_kw = {}
+    if args.norm:
+        from paper_2609_36452_amd.workload import round_bf16_bits
+        g = np.random.default_rng(args.seed + 7).uniform(0.5, 2.0, cfg.d)
+        gt = torch.from_numpy(round_bf16_bits(g)).view(torch.bfloat16) if cfg.dtype == "bf16" else \
+            torch.from_numpy(g.astype(np.float32))
+        norm_kw = dict(norm_weight=gt.to(dev), norm_eps=1e-5)
+    call = rpd.ScoreCommit(hidden, w_u, mask, P, max_masked=w.n_masked, **norm_kw)
     variant = rpd.projection_variant(cfg.K, cfg.B, cfg.L, cfg.d, cfg.V, hidden.dtype, max_masked=w.n_masked)
     log(f"projection variant {variant}")
     torch.cuda.synchronize()
@@ -244,13 +253,13 @@ def main() -> int:
                                f"masked={n} ({R} projected rows), rule={args.rule} beta={P.beta}"
                                + (f" block={P.block}" if P.block else ""),
                    "masked_positions": n, "projected_rows": R, "seed": args.seed,
-                   "commit_rule": "rpd_block" if P.block else "rpd"},
+                   "commit_rule": "rpd_block" if P.block else "rpd", "final_norm": bool(args.norm)},
         "iterations_per_s": round(1e3 / ms_step, 1),
         "roofline": roof,
     }
     if args.copy_probe:
         copy_probe(torch)
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.norm:
         import oracle as O
         OP = O.Params(**P.__dict__)
         log("cpu baseline (oracle)")

@@ -78,6 +78,20 @@ typedef enum rpd_status {
  *   w_u         device [V][d]; the unembedding (output head), d contiguous;
  *               16-byte aligned
  *   mask        device [B][L] uint8; nonzero = masked (in M_t)
+ *   norm_weight optional device [d], same type as hidden: the gain g of the
+ *               model's final normalization (RMS normalization). NULL: every
+ *               supplied state is already normalized and is projected as is.
+ *               Otherwise the states of layers 0 .. K-2 (and of layer K-1
+ *               too if norm_final != 0) are first replaced by
+ *               g * x / sqrt(mean(x^2) + norm_eps), evaluated in float64 and
+ *               rounded (to nearest, ties to even) to the input type, as the
+ *               model's normalization hands the output head (Appendix A.2
+ *               "Intermediate-layer readout", A.6 "Layerwise projection":
+ *               the final layer uses the native, already normalized state).
+ *               16-byte aligned for bf16.
+ *   norm_eps    >= 0, finite; the normalization's epsilon (unused without g)
+ *   norm_final  0: layer K-1 is the model's native normalized state (the
+ *               paper); 1: normalize it like the others
  *   max_masked  an upper bound on the number of masked positions summed over
  *               the batch, or -1. With -1 the call reads the exact count back
  *               from the device once (one stream synchronisation). If the
@@ -93,6 +107,9 @@ typedef struct rpd_problem {
   const void* w_u;
   const uint8_t* mask;
   int32_t max_masked;
+  const void* norm_weight;
+  float norm_eps;
+  int32_t norm_final;
 } rpd_problem;
 
 /*
@@ -112,6 +129,11 @@ typedef struct rpd_problem {
  * unused), and without one its most confident masked position is. The
  * reported upstream entropy is then the entropy over earlier masked
  * positions outside the commitment set.
+ *
+ * logit_scale multiplies every logit before the softmax statistics (an
+ * inverse temperature). The paper reads probabilities before any
+ * temperature (Appendix A.2), i.e. 1; 0 is read as 1; otherwise it must be
+ * finite and > 0. rpd_gate_commit ignores it.
  */
 typedef struct rpd_params {
   float theta_h;   /* high-confidence threshold (bypasses stability), Eq. 5 */
@@ -123,6 +145,7 @@ typedef struct rpd_params {
   int32_t window;  /* fallback window W, Section 3.2 */
   uint32_t flags;  /* reserved, must be 0 */
   int32_t block;   /* 0: full RPD; > 0: RPD-block with blocks of this many positions */
+  float logit_scale; /* inverse temperature of the scoring softmax; 0 or 1: none */
 } rpd_params;
 
 /*
@@ -165,7 +188,8 @@ typedef struct rpd_outputs {
 } rpd_outputs;
 
 /* Device workspace bytes that rpd_score_commit needs for problem `p`
- * (pointers in `p` are not read). Returns 0 if the shape is invalid. */
+ * (pointers in `p` are not read; norm_weight is only tested for NULL).
+ * Returns 0 if the shape is invalid. */
 size_t rpd_workspace_size(const rpd_problem* p);
 
 /*
@@ -180,7 +204,8 @@ rpd_status rpd_score_commit(const rpd_problem* p, const rpd_params* q, const rpd
  * rpd_score_commit, recording caller-created HIP events (hipEvent_t, cast to
  * void*) on `stream` at its stage boundaries, for callers that time the
  * stages: events[0] before the masked-position compaction, [1] before the
- * projection (logit lens + fused softmax statistics), [2] after it, [3]
+ * projection (logit lens + fused softmax statistics; with a norm_weight, the
+ * final normalization of the rows comes first, after [1]), [2] after it, [3]
  * after the cross-tile reduction and stability scoring, [4] after the
  * commitment scan (with B == 1 the commitment runs inside the reduction
  * kernel, so [3] and [4] coincide). Only the first n_events (0..5) are used;

@@ -34,13 +34,15 @@ class RpdProblem(ctypes.Structure):
     _fields_ = [("K", ctypes.c_int32), ("B", ctypes.c_int32), ("L", ctypes.c_int32),
                 ("d", ctypes.c_int32), ("V", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("hidden", ctypes.c_void_p), ("w_u", ctypes.c_void_p), ("mask", ctypes.c_void_p),
-                ("max_masked", ctypes.c_int32)]
+                ("max_masked", ctypes.c_int32), ("norm_weight", ctypes.c_void_p), ("norm_eps", ctypes.c_float),
+                ("norm_final", ctypes.c_int32)]
 
 
 class RpdParams(ctypes.Structure):
     _fields_ = [("theta_h", ctypes.c_float), ("theta_c", ctypes.c_float), ("theta_s", ctypes.c_float),
                 ("w", ctypes.c_float), ("k_max", ctypes.c_int32), ("beta", ctypes.c_float),
-                ("window", ctypes.c_int32), ("flags", ctypes.c_uint32), ("block", ctypes.c_int32)]
+                ("window", ctypes.c_int32), ("flags", ctypes.c_uint32), ("block", ctypes.c_int32),
+                ("logit_scale", ctypes.c_float)]
 
 
 _OUT_FIELDS = ["commit", "token", "entropy", "confidence", "persistence", "drop", "stability", "flags",
@@ -62,6 +64,7 @@ class Params:
     beta: float = 4.0
     window: int = 32
     block: int = 0     # 0: full RPD; > 0: RPD-block with blocks of this many positions
+    logit_scale: float = 1.0   # inverse temperature of the scoring softmax
 
     @staticmethod
     def llada() -> "Params":
@@ -79,7 +82,7 @@ class Params:
 
     def to_c(self) -> RpdParams:
         return RpdParams(self.theta_h, self.theta_c, self.theta_s, self.w, int(self.k_max), self.beta,
-                         int(self.window), 0, int(self.block))
+                         int(self.window), 0, int(self.block), float(self.logit_scale))
 
 
 class RpdError(RuntimeError):
@@ -153,14 +156,17 @@ def _dtype_code(t: torch.Tensor) -> int:
     raise TypeError(f"unsupported dtype {t.dtype} (bfloat16 or float32)")
 
 
-def make_problem(K, B, L, d, V, dtype_code, hidden=None, w_u=None, mask=None, max_masked=-1) -> RpdProblem:
-    return RpdProblem(K, B, L, d, V, dtype_code, _ptr(hidden), _ptr(w_u), _ptr(mask), int(max_masked))
+def make_problem(K, B, L, d, V, dtype_code, hidden=None, w_u=None, mask=None, max_masked=-1,
+                 norm_weight=None, norm_eps: float = 0.0, norm_final: bool = False) -> RpdProblem:
+    nw = norm_weight if isinstance(norm_weight, (int, type(None))) else _ptr(norm_weight)
+    return RpdProblem(K, B, L, d, V, dtype_code, _ptr(hidden), _ptr(w_u), _ptr(mask), int(max_masked),
+                      nw, float(norm_eps), int(bool(norm_final)))
 
 
 def workspace_size(K: int, B: int, L: int, d: int, V: int, dtype: torch.dtype | int,
-                   max_masked: int = -1) -> int:
+                   max_masked: int = -1, norm: bool = False) -> int:
     code = dtype if isinstance(dtype, int) else (DTYPE_BF16 if dtype == torch.bfloat16 else DTYPE_F32)
-    p = make_problem(K, B, L, d, V, code, max_masked=max_masked)
+    p = make_problem(K, B, L, d, V, code, max_masked=max_masked, norm_weight=1 if norm else None)
     return int(lib().rpd_workspace_size(ctypes.byref(p)))
 
 
@@ -228,15 +234,19 @@ class ScoreCommit:
     ``__call__`` only enqueues the library's kernels."""
 
     def __init__(self, hidden: torch.Tensor, w_u: torch.Tensor, mask: torch.Tensor, params: Params,
-                 max_masked: int | None = None, layer_stats: bool = False):
+                 max_masked: int | None = None, layer_stats: bool = False, norm_weight: torch.Tensor | None = None,
+                 norm_eps: float = 1e-5, norm_final: bool = False):
         K, B, L, d = hidden.shape
         V = w_u.shape[0]
         code = _dtype_code(hidden)
         _check_dev("hidden", hidden, (K, B, L, d), (hidden.dtype,))
         _check_dev("w_u", w_u, (V, d), (hidden.dtype,))
         _check_dev("mask", mask, (B, L), (torch.uint8, torch.bool))
+        if norm_weight is not None:
+            _check_dev("norm_weight", norm_weight, (d,), (hidden.dtype,))
         mm = -1 if max_masked is None else int(max_masked)
-        self.problem = make_problem(K, B, L, d, V, code, hidden, w_u, mask.view(torch.uint8), mm)
+        self.problem = make_problem(K, B, L, d, V, code, hidden, w_u, mask.view(torch.uint8), mm,
+                                    norm_weight, norm_eps, norm_final)
         self.params = params.to_c()
         self.out = alloc_outputs(K, B, L, hidden.device, layer_stats)
         self.out_c = _outputs_struct(self.out)
@@ -244,7 +254,7 @@ class ScoreCommit:
         if nbytes == 0:
             raise ValueError("invalid problem shape")
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=hidden.device)
-        self._keep = (hidden, w_u, mask)
+        self._keep = (hidden, w_u, mask, norm_weight)
 
     def __call__(self, stream=None, events=None) -> dict:
         """Enqueue one call. ``events``: optional list of up to five
@@ -264,13 +274,17 @@ class ScoreCommit:
 
 
 def score_commit(hidden: torch.Tensor, w_u: torch.Tensor, mask: torch.Tensor, params: Params,
-                 max_masked: int | None = None, layer_stats: bool = False, stream=None) -> dict:
+                 max_masked: int | None = None, layer_stats: bool = False, stream=None,
+                 norm_weight: torch.Tensor | None = None, norm_eps: float = 1e-5, norm_final: bool = False) -> dict:
     """``rpd_score_commit``: the whole commit step of one decoding iteration.
 
     hidden [K][B][L][d] and w_u [V][d] (bfloat16 or float32, same dtype,
-    device, contiguous), mask [B][L] uint8/bool. Returns the output tensors
-    (see include/rpd.h), valid once the stream has run."""
-    return ScoreCommit(hidden, w_u, mask, params, max_masked, layer_stats)(stream)
+    device, contiguous), mask [B][L] uint8/bool; optional norm_weight [d]
+    (the gain of the model's final normalization, applied to layers 0..K-2,
+    and to K-1 with norm_final). Returns the output tensors (see
+    include/rpd.h), valid once the stream has run."""
+    return ScoreCommit(hidden, w_u, mask, params, max_masked, layer_stats, norm_weight, norm_eps,
+                       norm_final)(stream)
 
 
 def gate_commit(mask: torch.Tensor, layer_argmax: torch.Tensor, layer_conf: torch.Tensor,

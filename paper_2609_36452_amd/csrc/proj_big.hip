@@ -1,4 +1,4 @@
-// K1 projection, bf16, large row counts (more than 192 projected rows): the
+// K1 projection, bf16, large row counts (more than 256 projected rows): the
 // MFMA-bound regime.
 #include "rpd_device.h"
 
@@ -40,7 +40,7 @@ constexpr int D = 2;   // chunks in flight in registers
 __global__ __launch_bounds__(256) void k_proj_bf16_big(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
-    int nvt, int nrt, int split_rows) {
+    int nvt, int nrt, int split_rows, const uint16_t* __restrict__ xrows, float scale) {
   using namespace big;
   static_assert(TV == 256 && TR == 256 && D == 2, "wave layout and register ring below assume these");
   __shared__ __attribute__((aligned(16))) uint16_t sa0[TV][KC], sa1[TV][KC];
@@ -69,11 +69,16 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     const int piece = (lane & 3) ^ ((tr >> 2) & 3);
     ga[u] = (long long)min(vb + tr, ve - 1) * d + piece * 8;
     const int r = r0 + tr < R ? r0 + tr : r0;   // padding rows re-read a real row; discarded at the end
-    const int p = r / K, l = r - p * K;
-    const int pos = rows[p];
-    const int b = pos / L, i = pos - b * L;
-    gb[u] = (((long long)l * B + b) * L + i) * (long long)d + piece * 8;
+    if (xrows) {   // normalized rows, already in projected-row order
+      gb[u] = (long long)r * d + piece * 8;
+    } else {
+      const int p = r / K, l = r - p * K;
+      const int pos = rows[p];
+      const int b = pos / L, i = pos - b * L;
+      gb[u] = (((long long)l * B + b) * L + i) * (long long)d + piece * 8;
+    }
   }
+  const uint16_t* __restrict__ xsrc = xrows ? xrows : hidden;
   const int srow = lane >> 2, scol = (lane & 3) * 8;
   // fragment reads: lane reads row base + (lane & 31), logical piece 2s + (lane >> 5)
   const int swl = ((lane & 31) >> 2) & 3;
@@ -94,7 +99,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     const long long k0_ = (long long)(chunk) * KC;                                                        \
     _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                                   \
       ld[slot][u_] = *reinterpret_cast<const u32x4*>(w_u + ga[u_] + k0_);                                 \
-      ld[slot][4 + u_] = *reinterpret_cast<const u32x4*>(hidden + gb[u_] + k0_);                          \
+      ld[slot][4 + u_] = *reinterpret_cast<const u32x4*>(xsrc + gb[u_] + k0_);                            \
     }                                                                                                     \
   } while (0)
 #define RPD_STORE(slot, stage)                                                                            \
@@ -174,7 +179,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
       const int piece = (lane & 3) ^ ((tr >> 2) & 3);
       const bool in = k0 + piece * 8 < d;
       const u32x4 va = in ? *reinterpret_cast<const u32x4*>(w_u + ga[u] + k0) : u32x4{0u, 0u, 0u, 0u};
-      const u32x4 vh = in ? *reinterpret_cast<const u32x4*>(hidden + gb[u] + k0) : u32x4{0u, 0u, 0u, 0u};
+      const u32x4 vh = in ? *reinterpret_cast<const u32x4*>(xsrc + gb[u] + k0) : u32x4{0u, 0u, 0u, 0u};
       *reinterpret_cast<u32x4*>(&sa0[tr][scol]) = va;
       *reinterpret_cast<u32x4*>(&sb0[tr][scol]) = vh;
     }
@@ -205,7 +210,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int v = vb + 128 * wv + 32 * mv + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
-        z[q] = acc[mv][nb][q];
+        z[q] = acc[mv][nb][q] * scale;
         vi[q] = v;
         ok[q] = v < ve;
       }
@@ -229,7 +234,8 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 hipError_t launch_proj_big(const Launch& a, hipStream_t s) {
   hipLaunchKernelGGL(k_proj_bf16_big, dim3(a.plan.grid), dim3(256), 0, s, static_cast<const uint16_t*>(a.hidden),
                      static_cast<const uint16_t*>(a.w_u), a.rows, a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V,
-                     a.plan.nvt, a.plan.nrt, a.plan.split_rows);
+                     a.plan.nvt, a.plan.nrt, a.plan.split_rows, static_cast<const uint16_t*>(a.xrows),
+                     a.logit_scale);
   return hipGetLastError();
 }
 

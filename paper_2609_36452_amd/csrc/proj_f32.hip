@@ -9,7 +9,8 @@ namespace {
 __global__ __launch_bounds__(256) void k_proj_f32(const float* __restrict__ hidden, const float* __restrict__ w_u,
                                                   const int32_t* __restrict__ rows,
                                                   const int32_t* __restrict__ n_ptr, float4* __restrict__ partials,
-                                                  int K, int B, int L, int d, int V, int nvt) {
+                                                  int K, int B, int L, int d, int V, int nvt,
+                                                  const float* __restrict__ xrows, float scale) {
   __shared__ float ws[64][33];
   __shared__ float xsm[16][33];
   __shared__ long long xoff[16];
@@ -24,10 +25,14 @@ __global__ __launch_bounds__(256) void k_proj_f32(const float* __restrict__ hidd
     const int r = r0 + tid;
     long long off = -1;
     if (r < R) {
-      const int p = r / K, l = r - p * K;
-      const int pos = rows[p];
-      const int b = pos / L, i = pos - b * L;
-      off = (((long long)l * B + b) * L + i) * (long long)d;
+      if (xrows) {   // normalized rows, already in projected-row order
+        off = (long long)r * d;
+      } else {
+        const int p = r / K, l = r - p * K;
+        const int pos = rows[p];
+        const int b = pos / L, i = pos - b * L;
+        off = (((long long)l * B + b) * L + i) * (long long)d;
+      }
     }
     xoff[tid] = off;
   }
@@ -42,7 +47,7 @@ __global__ __launch_bounds__(256) void k_proj_f32(const float* __restrict__ hidd
     for (int q = tid; q < 16 * 32; q += 256) {
       const int row = q >> 5, kk = q & 31;
       const long long off = xoff[row];
-      xsm[row][kk] = (off >= 0 && k0 + kk < d) ? hidden[off + k0 + kk] : 0.f;
+      xsm[row][kk] = (off >= 0 && k0 + kk < d) ? (xrows ? xrows : hidden)[off + k0 + kk] : 0.f;
     }
     __syncthreads();
 #pragma unroll 8
@@ -56,7 +61,7 @@ __global__ __launch_bounds__(256) void k_proj_f32(const float* __restrict__ hidd
   const int v = vb + lane;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    float z[1] = {acc[j]};
+    float z[1] = {acc[j] * scale};
     int vi[1] = {v};
     bool ok[1] = {v < ve};
     Soft st = soft_from_values(z, vi, ok);
@@ -72,7 +77,7 @@ __global__ __launch_bounds__(256) void k_proj_f32(const float* __restrict__ hidd
 hipError_t launch_proj_f32(const Launch& a, hipStream_t s) {
   hipLaunchKernelGGL(k_proj_f32, dim3(a.plan.grid), dim3(256), 0, s, static_cast<const float*>(a.hidden),
                      static_cast<const float*>(a.w_u), a.rows, a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V,
-                     a.plan.nvt);
+                     a.plan.nvt, static_cast<const float*>(a.xrows), a.logit_scale);
   return hipGetLastError();
 }
 

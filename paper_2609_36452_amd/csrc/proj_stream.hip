@@ -90,7 +90,7 @@ template <int NW, int MV, int NB, bool FC>
 __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
-    int nvt, int nrt, int split_rows, CompactArgs ca) {
+    int nvt, int nrt, int split_rows, CompactArgs ca, const uint16_t* __restrict__ xrows, float scale) {
   constexpr int TR = 32 * NB, WR = 32 * MV, KC = 64, NT = NW * 64;
   constexpr int NLD = WR / 8;          // W_U load instructions per wave per chunk
   constexpr int XLD = TR * 8 / NT;     // hidden-row pieces per thread per chunk
@@ -155,11 +155,16 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
     xrow[u] = row;
     xpiece[u] = (q & 7) ^ ((row >> 1) & 7);
     const int r = r0 + row < R ? r0 + row : r0;
-    const int p = r / K, l = r - p * K;
-    const int pos = FC ? s_pos[p] : rows[p];
-    const int b = pos / L, i = pos - b * L;
-    xa[u] = (((long long)l * B + b) * L + i) * (long long)d + xpiece[u] * 8;
+    if (xrows) {   // normalized rows, already in projected-row order
+      xa[u] = (long long)r * d + xpiece[u] * 8;
+    } else {
+      const int p = r / K, l = r - p * K;
+      const int pos = FC ? s_pos[p] : rows[p];
+      const int b = pos / L, i = pos - b * L;
+      xa[u] = (((long long)l * B + b) * L + i) * (long long)d + xpiece[u] * 8;
+    }
   }
+  const uint16_t* __restrict__ xsrc = xrows ? xrows : hidden;
   const int xpc = (tid & 7) * 8;       // LDS piece of this thread's hidden-row loads
   // fragments: row base + (lane & 31), logical piece 2s + (lane >> 5)
   const int fr = lane & 31, fsw = (fr >> 1) & 7, fhi = lane >> 5;
@@ -175,7 +180,7 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
   do {                                                                                                   \
     const long long k0_ = (long long)(chunk) * KC;                                                       \
     _Pragma("unroll") for (int u_ = 0; u_ < XLD; ++u_)                                                  \
-      xr[slot][u_] = *reinterpret_cast<const u32x4*>(hidden + xa[u_] + k0_);                             \
+      xr[slot][u_] = *reinterpret_cast<const u32x4*>(xsrc + xa[u_] + k0_);                               \
   } while (0)
 #define RPD_SLOAD(slot, chunk)                                                                           \
   do {                                                                                                   \
@@ -235,7 +240,7 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
 #pragma unroll
     for (int u = 0; u < XLD; ++u)
       *reinterpret_cast<u32x4*>(&xl[XS][xrow[u]][xpc]) =
-          k0 + xpiece[u] * 8 < d ? *reinterpret_cast<const u32x4*>(hidden + xa[u] + k0) : u32x4{0u, 0u, 0u, 0u};
+          k0 + xpiece[u] * 8 < d ? *reinterpret_cast<const u32x4*>(xsrc + xa[u] + k0) : u32x4{0u, 0u, 0u, 0u};
     __syncthreads();
     if (XS == 0)
       RPD_SMMA(0);
@@ -260,7 +265,7 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int v = vw + 32 * mv + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
-        z[q] = acc[mv][nb][q];
+        z[q] = acc[mv][nb][q] * scale;
         vi[q] = v;
         ok[q] = v < ve;
       }
@@ -289,11 +294,13 @@ void launch_stream(const Launch& a, hipStream_t s) {
   if (a.fused_compact)
     hipLaunchKernelGGL((k_proj_bf16_stream<NW, MV, NB, true>), dim3(p.grid), dim3(NW * 64), 0, s,
                        static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
-                       a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows, ca);
+                       a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows, ca,
+                       static_cast<const uint16_t*>(a.xrows), a.logit_scale);
   else
     hipLaunchKernelGGL((k_proj_bf16_stream<NW, MV, NB, false>), dim3(p.grid), dim3(NW * 64), 0, s,
                        static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
-                       a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows, ca);
+                       a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows, ca,
+                       static_cast<const uint16_t*>(a.xrows), a.logit_scale);
 }
 
 }  // namespace
@@ -302,7 +309,8 @@ bool compact_fused(const Launch& a) {
   const ProjVariant v = a.plan.variant;
   const bool streaming = v == PROJ_BF16_S32 || v == PROJ_BF16_S64 || v == PROJ_BF16_S128 || v == PROJ_BF16_S192 ||
                          v == PROJ_BF16_S256;
-  return streaming && a.plan.nrt == 1 && a.max_masked > 0 && (long long)a.B * a.L <= kFusedCompactMax;
+  return streaming && a.plan.nrt == 1 && a.max_masked > 0 && (long long)a.B * a.L <= kFusedCompactMax &&
+         !a.xrows;   // the normalization needs the row list before the projection
 }
 
 hipError_t launch_proj_stream(const Launch& a, hipStream_t s) {

@@ -39,6 +39,13 @@ long long masked_cap(const rpd_problem* p) {
 
 size_t partial_bytes(const rpd::ProjPlan& pl, long long rows) { return (size_t)rows * pl.nvt * 16; }
 
+size_t elem_bytes(const rpd_problem* p) { return p->dtype == RPD_DTYPE_BF16 ? 2 : 4; }
+
+// the normalized, compacted rows [K * cap][d] (only with a normalization)
+size_t norm_bytes(const rpd_problem* p, long long cap) {
+  return p->norm_weight ? align256((size_t)((long long)p->K * cap) * (size_t)p->d * elem_bytes(p)) : 0;
+}
+
 // Bytes for the plan chosen at `cap` masked positions; when the exact count
 // is read back later (max_masked < 0) any smaller count may be planned, so
 // the small-row variants are covered too.
@@ -52,7 +59,7 @@ size_t workspace_bytes_for(const rpd_problem* p, long long cap) {
       if (b > part) part = b;
     }
   }
-  return kHeaderBytes + align256((size_t)((long long)p->B * p->L) * 4) + align256(part);
+  return kHeaderBytes + align256((size_t)((long long)p->B * p->L) * 4) + align256(part) + norm_bytes(p, cap);
 }
 
 rpd_status check_params(const rpd_params* q) {
@@ -68,6 +75,8 @@ rpd_status check_params(const rpd_params* q) {
   if (q->window < 1) return fail(RPD_ERR_BAD_PARAM, "window must be >= 1 (got %d)", q->window);
   if (q->flags != 0) return fail(RPD_ERR_BAD_PARAM, "flags is reserved and must be 0");
   if (q->block < 0) return fail(RPD_ERR_BAD_PARAM, "block must be >= 0 (got %d)", q->block);
+  if (!std::isfinite(q->logit_scale) || q->logit_scale < 0.f)
+    return fail(RPD_ERR_BAD_PARAM, "logit_scale must be finite and > 0, or 0 for 1 (got %g)", q->logit_scale);
   return RPD_OK;
 }
 
@@ -91,6 +100,7 @@ void fill_common(rpd::Launch& a, const rpd_params* q, const rpd_outputs* o) {
   a.k_max = q->k_max;
   a.window = q->window;
   a.block = q->block;
+  a.logit_scale = q->logit_scale == 0.f ? 1.f : q->logit_scale;
   a.commit = o->commit;
   a.token = o->token;
   a.entropy = o->entropy;
@@ -139,6 +149,14 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
   } else if (((uintptr_t)p->hidden | (uintptr_t)p->w_u) & 3) {
     return fail(RPD_ERR_UNSUPPORTED, "fp32 hidden and w_u must be 4-byte aligned");
   }
+  if (p->norm_weight) {
+    if (((uintptr_t)p->norm_weight) & (p->dtype == RPD_DTYPE_BF16 ? 15 : 3))
+      return fail(RPD_ERR_UNSUPPORTED, "norm_weight must be aligned like hidden");
+    if (!std::isfinite(p->norm_eps) || p->norm_eps < 0.f)
+      return fail(RPD_ERR_BAD_PARAM, "norm_eps must be finite and >= 0 (got %g)", p->norm_eps);
+    if (p->norm_final != 0 && p->norm_final != 1)
+      return fail(RPD_ERR_BAD_PARAM, "norm_final must be 0 or 1 (got %d)", p->norm_final);
+  }
   rpd_status st = check_params(q);
   if (st != RPD_OK) return st;
   st = check_outputs(o);
@@ -170,6 +188,11 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
   a.done = reinterpret_cast<int32_t*>(ws + 8);
   a.rows = reinterpret_cast<int32_t*>(ws + kHeaderBytes);
   a.partials = reinterpret_cast<float4*>(ws + kHeaderBytes + align256((size_t)((long long)p->B * p->L) * 4));
+  a.norm_weight = p->norm_weight;
+  a.norm_eps = p->norm_eps;
+  a.norm_final = p->norm_final;
+  // the normalized rows sit at the end (the partials are sized for the largest plan)
+  a.xrows = p->norm_weight ? ws + (need - norm_bytes(p, cap)) : nullptr;
   fill_common(a, q, o);
 
   auto mark = [&](int k) -> hipError_t {
@@ -194,7 +217,8 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
     a.max_masked = n;
     a.plan = rpd::plan_projection(p->dtype, (long long)p->K * a.max_masked, p->V);
   }
-  if ((e = mark(1)) == hipSuccess && (e = rpd::launch_projection(a, s)) == hipSuccess && (e = mark(2)) == hipSuccess &&
+  if ((e = mark(1)) == hipSuccess && (!a.xrows || (e = rpd::launch_norm_rows(a, s)) == hipSuccess) &&
+      (e = rpd::launch_projection(a, s)) == hipSuccess && (e = mark(2)) == hipSuccess &&
       (e = rpd::launch_reduce_score(a, s)) == hipSuccess && (e = mark(3)) == hipSuccess &&
       (rpd::commit_fused(a) || (e = rpd::launch_commit(a, s)) == hipSuccess))
     e = mark(4);

@@ -55,11 +55,19 @@ struct Launch {
   bool fused_compact;    // the projection kernel does the compaction (no launch_compact)
   int32_t* rows;         // [max_masked] compacted b*L+i
   float4* partials;      // [K*max_masked][nvt]
+  // final normalization (norm_weight NULL: none): the projection then reads
+  // projected row r at xrows + r * d (normalized, compacted) instead of
+  // gathering it from hidden
+  const void* norm_weight;
+  float norm_eps;
+  int norm_final;
+  void* xrows;
   ProjPlan plan;
   // params
   float theta_h, theta_c, theta_s, w, beta;
   int k_max, window;
   int block;             // 0: full RPD; > 0: RPD-block
+  float logit_scale;     // multiplies every logit before the softmax statistics
   // outputs
   uint8_t* commit; int32_t* token; float* entropy; float* confidence;
   int32_t* persistence; float* drop; float* stability; uint8_t* flags;
@@ -82,6 +90,8 @@ bool commit_fused(const Launch& a);
 bool compact_fused(const Launch& a);
 
 // the projection variants, dispatched by launch_projection on a.plan.variant
+// the final normalization of the compacted rows into a.xrows (before the projection)
+hipError_t launch_norm_rows(const Launch& a, hipStream_t s);
 hipError_t launch_proj_stream(const Launch& a, hipStream_t s);  // PROJ_BF16_S32 .. PROJ_BF16_S256
 hipError_t launch_proj_big(const Launch& a, hipStream_t s);     // PROJ_BF16_BIG
 hipError_t launch_proj_f32(const Launch& a, hipStream_t s);     // PROJ_F32

@@ -32,12 +32,24 @@ def gpu_params(P: O.Params) -> rpd.Params:
     return rpd.Params(**dataclasses.asdict(P))
 
 
-def run_gpu(w, P: O.Params, layer_stats=True, max_masked="exact", tensors=None) -> dict:
+def gain_tensor(w, g: np.ndarray, dev="cuda:0") -> torch.Tensor:
+    """The normalization gain on the device, in the workload's input type."""
+    t = torch.from_numpy(np.ascontiguousarray(g))
+    return (t.view(torch.bfloat16) if w.cfg.dtype == "bf16" else t).to(dev)
+
+
+def run_gpu(w, P: O.Params, layer_stats=True, max_masked="exact", tensors=None, norm=None) -> dict:
+    """The HIP path through the C ABI; ``norm = (g, eps, norm_final)`` with g
+    in the input encoding (bf16 bit patterns or fp32)."""
     hidden, w_u, mask = tensors if tensors is not None else to_device(w)
     mm = w.n_masked if max_masked == "exact" else max_masked
     note(f"  gpu call: {w.cfg.name} K={w.cfg.K} B={w.cfg.B} L={w.cfg.L} d={w.cfg.d} V={w.cfg.V} "
-         f"dtype={w.cfg.dtype} n={w.n_masked} seed={w.seed} max_masked={mm}")
-    out = rpd.score_commit(hidden, w_u, mask, gpu_params(P), max_masked=mm, layer_stats=layer_stats)
+         f"dtype={w.cfg.dtype} n={w.n_masked} seed={w.seed} max_masked={mm}"
+         + (f" norm eps={norm[1]} final={norm[2]}" if norm else "") + f" scale={P.logit_scale}")
+    kw = {}
+    if norm is not None:
+        kw = dict(norm_weight=gain_tensor(w, norm[0], hidden.device), norm_eps=norm[1], norm_final=norm[2])
+    out = rpd.score_commit(hidden, w_u, mask, gpu_params(P), max_masked=mm, layer_stats=layer_stats, **kw)
     torch.cuda.synchronize()
     return {k: v.cpu().numpy() for k, v in out.items()}
 
@@ -45,12 +57,16 @@ def run_gpu(w, P: O.Params, layer_stats=True, max_masked="exact", tensors=None) 
 _LAYER_CACHE: dict = {}
 
 
-def run_oracle(w, P: O.Params) -> dict:
+def run_oracle(w, P: O.Params, norm=None) -> dict:
     """Oracle outputs; the per-layer projection of a workload is computed once
-    and reused across parameter sets."""
-    key = id(w)
+    per (normalization, logit scale) and reused across parameter sets. The
+    normalization epsilon is taken at float32, as the C ABI passes it."""
+    key = (id(w), None if norm is None else id(norm[0]), norm and (norm[1], norm[2]), P.logit_scale)
     if key not in _LAYER_CACHE or _LAYER_CACHE[key][0] is not w:
-        _LAYER_CACHE.clear()
-        _LAYER_CACHE[key] = (w, O.layer_stats_masked(w.hidden, w.w_u, w.mask, w.cfg.dtype))
+        if len(_LAYER_CACHE) > 8:
+            _LAYER_CACHE.clear()
+        onorm = None if norm is None else (norm[0], float(np.float32(norm[1])), bool(norm[2]))
+        _LAYER_CACHE[key] = (w, O.layer_stats_masked(w.hidden, w.w_u, w.mask, w.cfg.dtype, norm=onorm,
+                                                     logit_scale=P.logit_scale))
     pos, layer = _LAYER_CACHE[key][1]
     return O.assemble(w.mask, pos, layer, P)

@@ -30,9 +30,13 @@ def test_exports_every_declared_symbol():
         assert hasattr(L, n), n
 
 
-def test_params_struct_layout():
-    # rpd_params of include/rpd.h: eight 4-byte fields, then block
-    assert ctypes.sizeof(rpd.RpdParams) == 36 and rpd.RpdParams.block.offset == 32
+def test_struct_layouts():
+    # rpd_params of include/rpd.h: eight 4-byte fields, then block and logit_scale
+    assert ctypes.sizeof(rpd.RpdParams) == 40 and rpd.RpdParams.block.offset == 32
+    assert rpd.RpdParams.logit_scale.offset == 36
+    # rpd_problem: six ints, three pointers, max_masked, then the normalization fields
+    assert rpd.RpdProblem.norm_weight.offset == 56 and rpd.RpdProblem.norm_eps.offset == 64
+    assert ctypes.sizeof(rpd.RpdProblem) == 72
 
 
 def test_version_and_status_strings():
@@ -55,6 +59,9 @@ def test_workspace_size():
     # 100% masked: 1024 rows x 494 tiles of 256 vocabulary rows
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=256)
     assert n == 256 + 1024 + _a256(1024 * 494 * 16)
+    # with the final normalization: + the normalized rows (32 x 4096 bf16)
+    n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=8, norm=True)
+    assert n == 256 + 1024 + _a256(32 * 512 * 16) + 32 * 4096 * 2
     assert rpd.workspace_size(0, 1, 256, 4096, 126464, rpd.DTYPE_BF16) == 0
     assert rpd.workspace_size(65, 1, 256, 4096, 126464, rpd.DTYPE_BF16) == 0
     assert rpd.workspace_size(4, 1, 256, 4096, 126464, 7) == 0
@@ -85,14 +92,17 @@ def _fake_outputs():
 
 
 def _prob(**kw):
-    base = dict(K=4, B=1, L=256, d=4096, V=126464, dtype=0, hidden=4096, w_u=8192, mask=64, max_masked=8)
+    base = dict(K=4, B=1, L=256, d=4096, V=126464, dtype=0, hidden=4096, w_u=8192, mask=64, max_masked=8,
+                norm_weight=None, norm_eps=1e-5, norm_final=0)
     base.update(kw)
     return rpd.RpdProblem(base["K"], base["B"], base["L"], base["d"], base["V"], base["dtype"],
-                          base["hidden"], base["w_u"], base["mask"], base["max_masked"])
+                          base["hidden"], base["w_u"], base["mask"], base["max_masked"], base["norm_weight"],
+                          base["norm_eps"], base["norm_final"])
 
 
 def _params(**kw):
-    p = dict(theta_h=0.9, theta_c=0.6, theta_s=3.5, w=15.0, k_max=6, beta=4.0, window=32, flags=0, block=0)
+    p = dict(theta_h=0.9, theta_c=0.6, theta_s=3.5, w=15.0, k_max=6, beta=4.0, window=32, flags=0, block=0,
+             logit_scale=1.0)
     p.update(kw)
     return rpd.RpdParams(**p)
 
@@ -101,6 +111,8 @@ def _params(**kw):
     (dict(K=0), 2), (dict(K=65), 2), (dict(B=0), 2), (dict(L=0), 2), (dict(d=0), 2), (dict(V=0), 2),
     (dict(B=1 << 13, L=1 << 12), 2), (dict(dtype=3), 5), (dict(d=4100), 5), (dict(w_u=8200), 5),
     (dict(hidden=None), 1), (dict(mask=None), 1),
+    (dict(norm_weight=8200), 5), (dict(norm_weight=8192, norm_eps=-1.0), 3),
+    (dict(norm_weight=8192, norm_eps=math.nan), 3), (dict(norm_weight=8192, norm_final=2), 3),
 ])
 def test_problem_validation(kw, status):
     s, msg = _call(_prob(**kw), _params(), _fake_outputs())
@@ -110,7 +122,8 @@ def test_problem_validation(kw, status):
 
 @pytest.mark.parametrize("kw", [dict(theta_c=0.95), dict(theta_c=-0.1), dict(w=-1.0), dict(k_max=0),
                                 dict(beta=-1.0), dict(beta=math.nan), dict(window=0), dict(flags=1),
-                                dict(theta_h=math.nan), dict(theta_s=math.inf), dict(block=-1)])
+                                dict(theta_h=math.nan), dict(theta_s=math.inf), dict(block=-1),
+                                dict(logit_scale=-1.0), dict(logit_scale=math.inf)])
 def test_param_validation(kw):
     s, msg = _call(_prob(), _params(**kw), _fake_outputs())
     assert s == 3, msg

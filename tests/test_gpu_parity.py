@@ -8,6 +8,7 @@ k-chunk, and every projection variant (the streaming family at <= 32, 64,
 split across XCDs). Full-size LLaDA-8B / Dream-7B shapes are
 compared on sampled positions that the oracle computes one by one, plus the
 prefix-sum identity of the commitment on the GPU's own outputs."""
+import dataclasses
 import math
 
 import numpy as np
@@ -16,7 +17,7 @@ import torch
 
 import oracle as O
 from paper_2609_36452_amd import binding as rpd
-from paper_2609_36452_amd.workload import CONFIGS, draw_unembedding, make_workload
+from paper_2609_36452_amd.workload import CONFIGS, draw_unembedding, make_workload, round_bf16_bits
 from tests.gpu_util import gpu_params, note, run_gpu, run_oracle, to_device
 from tests.parity import compare, gap_tol, ENTROPY_TOL, CONF_TOL
 
@@ -29,9 +30,9 @@ def _need_gpu():
         pytest.skip("no GPU")
 
 
-def _check(w, P, layer=True, **kw):
-    g = run_gpu(w, P, layer_stats=layer, **kw)
-    o = run_oracle(w, P)
+def _check(w, P, layer=True, norm=None, **kw):
+    g = run_gpu(w, P, layer_stats=layer, norm=norm, **kw)
+    o = run_oracle(w, P, norm=norm)
     rep = compare(g, o, w.mask, P, w.cfg.d, layer=layer)
     note("  " + rep.summary()[:300])
     assert rep.ok(), rep.summary()
@@ -104,6 +105,45 @@ def test_rpd_block_at_late_decode_shape():
     # the headline shape with the paper's block size
     w = make_workload("llada_late", 3)
     _check(w, O.Params(theta_s=3.5, w=15.0, block=32))
+
+
+# ------------------------------------------- final normalization, scale --
+
+def _gain(w, seed):
+    # the normalization gain, g ~ U(0.5, 2), in the workload's input encoding
+    g = np.random.default_rng(seed).uniform(0.5, 2.0, w.cfg.d)
+    return round_bf16_bits(g) if w.cfg.dtype == "bf16" else g.astype(np.float32)
+
+
+NORM_CASES = [c for c in BF16_CASES if c[0] in ("bf16_s32", "bf16_s128_long_d", "bf16_s256_odd_chunks",
+                                               "bf16_big_vocab_split")]
+
+
+@pytest.mark.parametrize("name,ov,seed", NORM_CASES, ids=[c[0] for c in NORM_CASES])
+@pytest.mark.parametrize("norm_final", [False, True])
+def test_final_normalization_prologue(name, ov, seed, norm_final):
+    # Appendix A.2 "Intermediate-layer readout": layers 0..K-2 through the final normalization,
+    # the final layer native unless norm_final
+    base = CONFIGS["llada_late"].with_(name=name, **ov).with_(sharp=("calibrated",), unstable_frac=0.3)
+    w = make_workload(base, seed)
+    norm = (_gain(w, seed + 100), 1e-5, norm_final)
+    for P in (O.LLADA, O.strict(base.K, 1.0)):
+        _check(w, P, norm=norm)
+
+
+@pytest.mark.parametrize("scale", [0.5, 2.0])
+@pytest.mark.parametrize("name", ["bf16_s32", "bf16_s128_long_d", "bf16_big_vocab_split"])
+def test_logit_scale(name, scale):
+    ov, seed = {c[0]: (c[1], c[2]) for c in BF16_CASES}[name]
+    w = make_workload(CONFIGS["llada_late"].with_(name=name, **ov), seed)
+    _check(w, dataclasses.replace(O.DREAM, logit_scale=scale))
+
+
+def test_fp32_normalization_and_scale():
+    w = make_workload("tiny", 7)
+    norm = (_gain(w, 9), 1e-6, False)
+    _check(w, dataclasses.replace(O.strict(3, 1.0), logit_scale=1.5), norm=norm)
+    _check(w, O.LLADA, norm=(norm[0], 0.0, True))
 
 
 # ------------------------------------------------------------- edge cases --
