@@ -25,7 +25,9 @@ Every function follows a passage of the paper (He, Liu, Xiong, Zhang,
   Table 4 (Appendix A.6);
 * the RPD-block commitment -- Section 3.2 "Variants" and Appendix A.6
   "RPD-block": the candidates of the active 32-position block, no budget,
-  fallback to the block's most confident masked position.
+  fallback to the block's most confident masked position;
+* lazy layerwise projection -- Appendix A.6 "Layerwise projection": layers
+  are projected only until a position's agreement suffix is determined.
 
 Readings where the paper is silent (stated once here, used throughout):
 the supplied hidden states are already normalised (the projection is a plain
@@ -395,6 +397,72 @@ def select(mask: np.ndarray, layer: dict, p: Params, positions: list[tuple[int, 
         if sc["fallback"] >= 0:
             o["flags"][b, masked[sc["fallback"]]] |= FLAG_FALLBACK
         o["n_commit"][b] = int(sc["commit"].sum())
+    return o
+
+
+def lazy_layer_stats(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params,
+                     norm: tuple | None = None):
+    """Lazy layerwise projection (Appendix A.6 "Layerwise projection": layers
+    are materialized only until the agreement suffix of a position is
+    determined). The final layer of every masked position is projected first.
+    Only a position whose candidacy the stability test can decide
+    (theta_c <= c < theta_h, Eq. 5) projects intermediate layers, from K-2
+    downwards, stopping after the first layer whose argmax differs from the
+    final token; its persistence and drop are then exactly those of the eager
+    projection. Unprojected layers hold argmax -1 and NaN statistics.
+    Returns (positions, per-layer statistics, layers projected per position)."""
+    pos = masked_positions(mask)
+    K = hidden.shape[0]
+    n = len(pos)
+    layer = {k: np.full((n, K), np.nan) for k in ("conf", "entropy", "p_final", "gap", "absbound")}
+    layer["argmax"] = np.full((n, K), -1, np.int64)
+    projected = np.zeros(n, np.int64)
+
+    def one(a: int, l: int) -> dict:
+        # layer l of position a alone; normalized like the eager path (layer K-1 native unless norm_final)
+        b, i = pos[a]
+        hl = hidden[l:l + 1]
+        nrm = None
+        if norm is not None and (l < K - 1 or norm[2]):
+            nrm = (norm[0], norm[1], True)
+        st = project_layer_stats(hl, w_u, dtype, [(b, i)], norm=nrm, logit_scale=p.logit_scale)
+        projected[a] += 1
+        return {k: st[k][0, 0] for k in ("argmax", "conf", "entropy", "gap", "absbound")}
+
+    for a in range(n):
+        f = one(a, K - 1)
+        for k in ("argmax", "conf", "entropy", "gap", "absbound"):
+            layer[k][a, K - 1] = f[k]
+        layer["p_final"][a, K - 1] = f["conf"]
+        c = f["conf"]
+        if not (p.theta_c <= c < p.theta_h):
+            continue
+        for l in range(K - 2, -1, -1):
+            st = one(a, l)
+            for k in ("argmax", "conf", "entropy", "gap", "absbound"):
+                layer[k][a, l] = st[k]
+            if st["argmax"] != f["argmax"]:
+                break
+            layer["p_final"][a, l] = st["conf"]   # the layer's argmax is the final token
+    return pos, layer, projected
+
+
+def score_commit_lazy(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params,
+                      norm: tuple | None = None) -> dict:
+    """The commit step with lazy layerwise projection: the same candidacy and
+    commitment as score_commit (stability matters only inside the band
+    theta_c <= c < theta_h, where the walk reaches the first disagreement).
+    Outside the band stability is not evaluated: persistence -1, drop and
+    stability NaN. ``layers_projected`` counts the projections per position."""
+    pos, layer, projected = lazy_layer_stats(hidden, w_u, mask, dtype, p, norm)
+    o = assemble(mask, pos, layer, p)
+    for a, (b, i) in enumerate(pos):
+        c = layer["conf"][a, -1]
+        if not (p.theta_c <= c < p.theta_h):
+            o["persistence"][b, i] = -1
+            o["drop"][b, i] = np.nan
+            o["stability"][b, i] = np.nan
+    o["layers_projected"] = projected
     return o
 
 

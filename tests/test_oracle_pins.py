@@ -539,3 +539,46 @@ def test_logit_scale_is_a_softmax_temperature():
     # a sharper distribution has lower entropy
     sharp = O.project_layer_stats(w.hidden, w.w_u, w.cfg.dtype, pos, logit_scale=4.0)
     assert (sharp["entropy"] <= base["entropy"] + 1e-12).all()
+
+
+# ------------------------------------------------------- lazy projection ----
+# Appendix A.6 "Layerwise projection": layers are projected only until the
+# agreement suffix of a position is determined.
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("pname", ["llada", "dream"])
+def test_lazy_projection_keeps_every_decision(seed, pname):
+    cfg = CONFIGS["tiny"].with_(sharp=("calibrated",), unstable_frac=0.4)
+    w = make_workload(cfg, 300 + seed)
+    P = O.LLADA if pname == "llada" else O.DREAM
+    eager = O.score_commit(w.hidden, w.w_u, w.mask, w.cfg.dtype, P)
+    lazy = O.score_commit_lazy(w.hidden, w.w_u, w.mask, w.cfg.dtype, P)
+    m = w.mask != 0
+    # one row at a time versus batched products: floats agree to rounding, decisions exactly
+    for k in ("commit", "token", "flags", "n_commit"):
+        np.testing.assert_array_equal(lazy[k], eager[k], err_msg=k)
+    for k in ("entropy", "confidence", "upstream_entropy"):
+        np.testing.assert_allclose(lazy[k], eager[k], rtol=1e-12, atol=1e-12, err_msg=k)
+    band = m & (eager["confidence"] >= P.theta_c) & (eager["confidence"] < P.theta_h)
+    np.testing.assert_array_equal(lazy["persistence"][band], eager["persistence"][band])
+    for k in ("drop", "stability"):
+        np.testing.assert_allclose(lazy[k][band], eager[k][band], rtol=1e-12, atol=1e-12, err_msg=k)
+    assert (lazy["persistence"][m & ~band] == -1).all() and np.isnan(lazy["stability"][m & ~band]).all()
+    # layers projected: 1 outside the band; inside it every agreeing layer plus the first disagreeing one
+    K = w.cfg.K
+    pos = O.masked_positions(w.mask)
+    for a, (b, i) in enumerate(pos):
+        want = min(K, eager["persistence"][b, i] + 1) if band[b, i] else 1
+        assert lazy["layers_projected"][a] == want, (b, i)
+    assert lazy["layers_projected"].sum() < K * len(pos)
+
+
+def test_lazy_projection_with_normalization():
+    w = make_workload(CONFIGS["tiny"].with_(sharp=("calibrated",)), 311)
+    g = np.random.default_rng(5).uniform(0.5, 2.0, w.cfg.d).astype(np.float32)
+    for final in (False, True):
+        norm = (g, 1e-6, final)
+        eager = O.score_commit(w.hidden, w.w_u, w.mask, w.cfg.dtype, O.LLADA, norm=norm)
+        lazy = O.score_commit_lazy(w.hidden, w.w_u, w.mask, w.cfg.dtype, O.LLADA, norm=norm)
+        for k in ("commit", "token", "flags"):
+            np.testing.assert_array_equal(lazy[k], eager[k], err_msg=k)
