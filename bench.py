@@ -136,6 +136,8 @@ def main() -> int:
     ap.add_argument("--beta", type=float, default=1.0)
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--lazy", action="store_true",
+                    help="lazy layerwise projection (intermediate layers only where stability decides)")
     ap.add_argument("--norm", action="store_true",
                     help="pass a normalization gain: layers 0..K-2 go through the final normalization first")
     ap.add_argument("--copy-probe", action="store_true",
@@ -168,6 +170,8 @@ def main() -> int:
         P = dataclasses.replace(rpd.Params.llada(), block=32)
     else:
         P = rpd.Params.dream()
+    if args.lazy:
+        P = dataclasses.replace(P, lazy=True)
     dev = torch.device("cuda:0")
     if cfg.dtype == "bf16":
         hidden = torch.from_numpy(w.hidden).view(torch.bfloat16).to(dev)
@@ -253,7 +257,8 @@ def main() -> int:
                                f"masked={n} ({R} projected rows), rule={args.rule} beta={P.beta}"
                                + (f" block={P.block}" if P.block else ""),
                    "masked_positions": n, "projected_rows": R, "seed": args.seed,
-                   "commit_rule": "rpd_block" if P.block else "rpd", "final_norm": bool(args.norm)},
+                   "commit_rule": "rpd_block" if P.block else "rpd", "final_norm": bool(args.norm),
+                   "lazy_projection": bool(P.lazy)},
         "iterations_per_s": round(1e3 / ms_step, 1),
         "roofline": roof,
     }

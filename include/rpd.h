@@ -52,6 +52,9 @@ typedef enum rpd_status {
   RPD_ERR_HIP = 6                  /* a HIP runtime call or launch failed */
 } rpd_status;
 
+/* bits of rpd_params.flags */
+#define RPD_PARAM_LAZY 1u /* lazy layerwise projection (see rpd_params) */
+
 /* per-position flag bits written to rpd_outputs.flags */
 #define RPD_FLAG_CANDIDATE 1u  /* in the candidate set C_t (Eq. 5) */
 #define RPD_FLAG_HIGH_CONF 2u  /* admitted because c_i >= theta_h */
@@ -116,8 +119,8 @@ typedef struct rpd_problem {
  * Hyperparameters (Table 4, Appendix A.6; LLaDA: theta_s 3.5, w 15; Dream:
  * theta_s 2.5, w 20; both theta_h 0.9, theta_c 0.6, K_max 6, beta 4 nats,
  * W 32). Requirements: 0 <= theta_c <= theta_h, w >= 0, k_max >= 1,
- * beta >= 0 (may be +inf), window >= 1, flags == 0 (reserved), block >= 0;
- * no NaN.
+ * beta >= 0 (may be +inf), window >= 1, flags only RPD_PARAM_LAZY,
+ * block >= 0; no NaN.
  *
  * block selects the commitment rule. 0: full RPD (Section 3.2), the
  * cumulative-entropy budget beta over the whole canvas with the fallback
@@ -129,6 +132,20 @@ typedef struct rpd_problem {
  * unused), and without one its most confident masked position is. The
  * reported upstream entropy is then the entropy over earlier masked
  * positions outside the commitment set.
+ *
+ * RPD_PARAM_LAZY in flags: lazy layerwise projection (Appendix A.6
+ * "Layerwise projection": layers are projected only until a position's
+ * agreement suffix is determined). The final layer of every masked position
+ * is projected first; intermediate layers only for positions with
+ * theta_c <= c < theta_h (the only ones whose candidacy stability decides,
+ * Eq. 5), from layer K-2 down, each stopping after its first disagreeing
+ * layer. Tokens, candidacy and commitment are those of the eager projection,
+ * and so are persistence, drop and stability inside that band; outside it
+ * they are not evaluated (persistence -1, drop and stability NaN), and the
+ * per-layer outputs of layers never projected hold -1 / NaN. One projection
+ * pass per layer (each streams W_U again) and one stream synchronisation
+ * per pass after the first: it pays where the projection is compute-bound
+ * (many masked positions), not where streaming W_U dominates.
  *
  * logit_scale multiplies every logit before the softmax statistics (an
  * inverse temperature). The paper reads probabilities before any
@@ -143,7 +160,7 @@ typedef struct rpd_params {
   int32_t k_max;   /* cap on persistence, Eq. 4 */
   float beta;      /* cumulative entropy budget in nats, Section 3.2 */
   int32_t window;  /* fallback window W, Section 3.2 */
-  uint32_t flags;  /* reserved, must be 0 */
+  uint32_t flags;  /* RPD_PARAM_* bits */
   int32_t block;   /* 0: full RPD; > 0: RPD-block with blocks of this many positions */
   float logit_scale; /* inverse temperature of the scoring softmax; 0 or 1: none */
 } rpd_params;
@@ -209,7 +226,9 @@ rpd_status rpd_score_commit(const rpd_problem* p, const rpd_params* q, const rpd
  * after the cross-tile reduction and stability scoring, [4] after the
  * commitment scan (with B == 1 the commitment runs inside the reduction
  * kernel, so [3] and [4] coincide). Only the first n_events (0..5) are used;
- * NULL entries are skipped. Everything else is exactly rpd_score_commit.
+ * NULL entries are skipped (with RPD_PARAM_LAZY, [1] precedes the first
+ * pass and [2] follows the last). Everything else is exactly
+ * rpd_score_commit.
  */
 rpd_status rpd_score_commit_timed(const rpd_problem* p, const rpd_params* q, const rpd_outputs* o,
                                   void* workspace, size_t workspace_bytes, void* stream,

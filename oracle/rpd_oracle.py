@@ -76,6 +76,7 @@ class Params:
     window: int = 32         # fallback window W
     block: int = 0           # 0: full RPD; > 0: RPD-block with blocks of this many positions
     logit_scale: float = 1.0  # multiplies every logit before the softmax statistics (1 / temperature)
+    lazy: bool = False        # lazy layerwise projection (score_commit_lazy); the rule itself is unchanged
 
 
 LLADA = Params(theta_s=3.5, w=15.0)

@@ -25,6 +25,7 @@ FLAG_COMMITTED = 8
 FLAG_FALLBACK = 16
 
 DEVICE_STATUS_MASKED_OVERFLOW = 1
+PARAM_LAZY = 1
 
 STATUS_NAMES = {0: "RPD_OK", 1: "RPD_ERR_NULL_POINTER", 2: "RPD_ERR_BAD_SHAPE", 3: "RPD_ERR_BAD_PARAM",
                 4: "RPD_ERR_WORKSPACE_TOO_SMALL", 5: "RPD_ERR_UNSUPPORTED", 6: "RPD_ERR_HIP"}
@@ -65,6 +66,7 @@ class Params:
     window: int = 32
     block: int = 0     # 0: full RPD; > 0: RPD-block with blocks of this many positions
     logit_scale: float = 1.0   # inverse temperature of the scoring softmax
+    lazy: bool = False         # lazy layerwise projection (RPD_PARAM_LAZY)
 
     @staticmethod
     def llada() -> "Params":
@@ -82,7 +84,8 @@ class Params:
 
     def to_c(self) -> RpdParams:
         return RpdParams(self.theta_h, self.theta_c, self.theta_s, self.w, int(self.k_max), self.beta,
-                         int(self.window), 0, int(self.block), float(self.logit_scale))
+                         int(self.window), PARAM_LAZY if self.lazy else 0, int(self.block),
+                         float(self.logit_scale))
 
 
 class RpdError(RuntimeError):

@@ -1,0 +1,180 @@
+// Lazy layerwise projection (Appendix A.6 "Layerwise projection": layers are
+// materialized only until the agreement suffix of a position is determined).
+//
+// The host drives one pass per layer, from the final layer down:
+//   pass 0      the final layer of every masked position;
+//   pass t > 0  layer K-1-t of the positions still "alive": those whose
+//               final confidence lies in the band theta_c <= c < theta_h
+//               (the only ones whose candidacy the stability test decides,
+//               Eq. 5) and whose layers K-t .. K-1 all agreed with the final
+//               token.
+// Each pass is the ordinary projection over an explicit list of rows (a
+// table of element offsets into the hidden states, or normalized rows),
+// followed by k_lazy_reduce (merge the tile states, update each position's
+// suffix length and peak probability) and k_lazy_next (list the positions
+// still alive with the row offsets of the next layer; the host reads their
+// count back to plan the next pass and stops at zero). k_lazy_score then
+// evaluates Eq. 2-5 from the per-position state, with persistence exact for
+// every position of the band; outside it stability is not evaluated
+// (persistence -1, drop and stability NaN). The commitment follows as usual.
+#include "rpd_device.h"
+
+namespace rpd {
+namespace {
+
+// fixed-order merge of one row's nvt tile states by one wave (as the eager
+// reduction does)
+__device__ __forceinline__ Soft lazy_merge_row(const float4* __restrict__ src, int nvt, int lane) {
+  const float4 empty = soft_pack(soft_empty());
+  Soft s = soft_empty();
+  for (int t0 = lane; t0 < nvt; t0 += 64 * 8) {
+    float4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = (t0 + 64 * u < nvt) ? src[t0 + 64 * u] : empty;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s = soft_merge(s, soft_unpack(v[u]));
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) s = soft_merge(s, soft_shfl_xor(s, m));
+  return s;
+}
+
+// one wave per row j < m of the pass (layer l): statistics of the row, then
+// the update of its position's state
+__global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ partials, int nvt,
+                                                    const int32_t* __restrict__ m_ptr, LazyState st, int l, int K,
+                                                    int B, int L, const int32_t* __restrict__ rows, float theta_c,
+                                                    float theta_h, int32_t* __restrict__ layer_argmax,
+                                                    float* __restrict__ layer_conf, float* __restrict__ layer_entropy) {
+  const int j = blockIdx.x, lane = threadIdx.x;
+  if (j >= *m_ptr) return;
+  const Soft s = lazy_merge_row(partials + (long long)j * nvt, nvt, lane);
+  if (lane != 0) return;
+  const int y = (s.idx == INT_MAX) ? -1 : s.idx;
+  const float c = 1.0f / s.S;
+  const float h = (s.S != s.S) ? s.S : fmaxf(logf(s.S) - s.T / s.S, 0.0f);
+  const int p = st.act[j];
+  if (l == K - 1) {
+    st.y[p] = y;
+    st.c[p] = c;
+    st.h[p] = h;
+    st.k[p] = 1;
+    st.pmax[p] = c;
+    st.alive[p] = (K > 1 && c >= theta_c && c < theta_h) ? 1 : 0;   // NaN fails
+  } else if (y == st.y[p]) {
+    st.k[p] += 1;
+    st.pmax[p] = fmaxf(st.pmax[p], c);
+    st.alive[p] = l > 0 ? 1 : 0;
+  } else {
+    st.alive[p] = 0;
+  }
+  st.depth[p] = K - l;
+  if (layer_argmax) {
+    const int pos = rows[p];
+    const int b = pos / L, i = pos - b * L;
+    const long long ol = ((long long)l * B + b) * L + i;
+    layer_argmax[ol] = y;
+    layer_conf[ol] = c;
+    layer_entropy[ol] = h;
+  }
+}
+
+// one workgroup: the positions still alive, in order, with the element
+// offsets of their layer-l rows; the count goes to *m_out. With first != 0
+// every position p < n is listed (the final-layer pass).
+constexpr int kLazyNextThreads = 1024;
+__global__ __launch_bounds__(kLazyNextThreads) void k_lazy_next(const int32_t* __restrict__ n_ptr, LazyState st,
+                                                                const int32_t* __restrict__ rows, int l, int first,
+                                                                int B, int L, int d, int32_t* __restrict__ m_out) {
+  __shared__ int wsum[kLazyNextThreads / 64];
+  const int n = *n_ptr;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int carry = 0;
+  for (int base = 0; base < n; base += blockDim.x) {
+    const int p = base + threadIdx.x;
+    const bool f = p < n && (first || st.alive[p] != 0);
+    const unsigned long long bal = __ballot(f);
+    const int before = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[wid] = __popcll(bal);
+    __syncthreads();
+    int off = 0, tot = 0;
+    for (int w = 0; w < nw; ++w) {
+      const int c = wsum[w];
+      off += (w < wid) ? c : 0;
+      tot += c;
+    }
+    if (f) {
+      const int j = carry + off + before;
+      const int pos = rows[p];
+      const int b = pos / L, i = pos - b * L;
+      st.act[j] = p;
+      st.rowoff[j] = (((long long)l * B + b) * L + i) * (long long)d;
+    }
+    carry += tot;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *m_out = carry;
+}
+
+// Eq. 2-5 from the per-position state, one thread per masked position
+__global__ __launch_bounds__(256) void k_lazy_score(const int32_t* __restrict__ n_ptr, LazyState st,
+                                                    const int32_t* __restrict__ rows, LazyScoreArgs a) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= *n_ptr) return;
+  const int pos = rows[p];
+  const int b = pos / a.L, i = pos - b * a.L;
+  const long long o = (long long)b * a.L + i;
+  const float c = st.c[p];
+  const bool band = c >= a.theta_c && c < a.theta_h;
+  const bool high = c >= a.theta_h;
+  float r = NAN, s = NAN;
+  int k = -1;
+  bool stab = false;
+  if (band) {
+    k = st.k[p];
+    r = st.pmax[p] - c;
+    s = fmaf(-a.w, r, (float)min(k, a.k_max));
+    stab = s >= a.theta_s;
+  }
+  a.token[o] = st.y[p];
+  a.entropy[o] = st.h[p];
+  a.confidence[o] = c;
+  a.persistence[o] = k;
+  a.drop[o] = r;
+  a.stability[o] = s;
+  a.flags[o] = (uint8_t)((high || stab ? kFlagCandidate : 0u) | (high ? kFlagHigh : 0u) | (stab ? kFlagStable : 0u));
+  if (a.layer_argmax)   // layers never projected
+    for (int l = 0; l < a.K - st.depth[p]; ++l) {
+      const long long ol = ((long long)l * a.B + b) * a.L + i;
+      a.layer_argmax[ol] = -1;
+      a.layer_conf[ol] = NAN;
+      a.layer_entropy[ol] = NAN;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_lazy_next(const Launch& a, int l, int first, hipStream_t s) {
+  hipLaunchKernelGGL(k_lazy_next, dim3(1), dim3(kLazyNextThreads), 0, s, a.n_masked, a.lazy, a.rows, l, first, a.B,
+                     a.L, a.d, a.lazy.m);
+  return hipGetLastError();
+}
+
+hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, hipStream_t s) {
+  if (m_cap <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_lazy_reduce, dim3(m_cap), dim3(64), 0, s, a.partials, a.plan.nvt, a.lazy.m, a.lazy, l, a.K,
+                     a.B, a.L, a.rows, a.theta_c, a.theta_h, a.layer_argmax, a.layer_conf, a.layer_entropy);
+  return hipGetLastError();
+}
+
+hipError_t launch_lazy_score(const Launch& a, hipStream_t s) {
+  if (a.max_masked <= 0) return hipSuccess;
+  LazyScoreArgs sa{a.K,          a.B,          a.L,         a.theta_h,     a.theta_c,    a.theta_s,
+                   a.w,          a.k_max,      a.token,     a.entropy,     a.confidence, a.persistence,
+                   a.drop,       a.stability,  a.flags,     a.layer_argmax, a.layer_conf, a.layer_entropy};
+  hipLaunchKernelGGL(k_lazy_score, dim3((unsigned)((a.max_masked + 255) / 256)), dim3(256), 0, s, a.n_masked,
+                     a.lazy, a.rows, sa);
+  return hipGetLastError();
+}
+
+}  // namespace rpd

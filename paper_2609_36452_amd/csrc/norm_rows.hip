@@ -49,18 +49,31 @@ __device__ __forceinline__ void store_f64(float* p, long long k, double v) { p[k
 constexpr int kNormThreads = 256;
 
 // one workgroup per projected row r = p*K + l (r < n*K)
+// With an explicit row list (rowoff, a lazy pass over layer pass_layer),
+// row r < *n_ptr is hidden + rowoff[r]; otherwise rows are gathered for
+// r < *n_ptr * K.
 template <typename T>
 __global__ __launch_bounds__(kNormThreads) void k_norm_rows(const T* __restrict__ hidden, const T* __restrict__ g,
                                                            const int32_t* __restrict__ rows,
                                                            const int32_t* __restrict__ n_ptr, T* __restrict__ xrows,
-                                                           int K, int B, int L, int d, float eps, int norm_final) {
+                                                           int K, int B, int L, int d, float eps, int norm_final,
+                                                           const long long* __restrict__ rowoff, int pass_layer) {
   __shared__ double s_ss[kNormThreads / 64];
   const int r = blockIdx.x;
-  if (r >= *n_ptr * K) return;
-  const int p = r / K, l = r - p * K;
-  const int pos = rows[p];
-  const int b = pos / L, i = pos - b * L;
-  const T* src = hidden + (((long long)l * B + b) * L + i) * (long long)d;
+  int l;
+  const T* src;
+  if (rowoff) {
+    if (r >= *n_ptr) return;
+    l = pass_layer;
+    src = hidden + rowoff[r];
+  } else {
+    if (r >= *n_ptr * K) return;
+    const int p = r / K;
+    l = r - p * K;
+    const int pos = rows[p];
+    const int b = pos / L, i = pos - b * L;
+    src = hidden + (((long long)l * B + b) * L + i) * (long long)d;
+  }
   T* dst = xrows + (long long)r * d;
   if (l == K - 1 && !norm_final) {
     for (int k = threadIdx.x; k < d; k += kNormThreads) dst[k] = src[k];
@@ -87,15 +100,18 @@ __global__ __launch_bounds__(kNormThreads) void k_norm_rows(const T* __restrict_
 
 hipError_t launch_norm_rows(const Launch& a, hipStream_t s) {
   if (a.max_masked <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((long long)a.K * a.max_masked));
+  // an explicit row list holds max_masked rows
+  const dim3 grid((unsigned)(a.rowoff ? (long long)a.max_masked : (long long)a.K * a.max_masked));
+  const int K = a.K;
   if (a.plan.variant == PROJ_F32)
     hipLaunchKernelGGL(k_norm_rows<float>, grid, dim3(kNormThreads), 0, s, static_cast<const float*>(a.hidden),
                        static_cast<const float*>(a.norm_weight), a.rows, a.n_masked, static_cast<float*>(a.xrows),
-                       a.K, a.B, a.L, a.d, a.norm_eps, a.norm_final);
+                       K, a.B, a.L, a.d, a.norm_eps, a.norm_final, a.rowoff, a.pass_layer);
   else
     hipLaunchKernelGGL(k_norm_rows<uint16_t>, grid, dim3(kNormThreads), 0, s,
                        static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.norm_weight), a.rows,
-                       a.n_masked, static_cast<uint16_t*>(a.xrows), a.K, a.B, a.L, a.d, a.norm_eps, a.norm_final);
+                       a.n_masked, static_cast<uint16_t*>(a.xrows), K, a.B, a.L, a.d, a.norm_eps, a.norm_final,
+                       a.rowoff, a.pass_layer);
   return hipGetLastError();
 }
 

@@ -40,7 +40,8 @@ constexpr int D = 2;   // chunks in flight in registers
 __global__ __launch_bounds__(256) void k_proj_bf16_big(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
-    int nvt, int nrt, int split_rows, const uint16_t* __restrict__ xrows, float scale) {
+    int nvt, int nrt, int split_rows, const uint16_t* __restrict__ xrows, const long long* __restrict__ rowoff,
+    float scale) {
   using namespace big;
   static_assert(TV == 256 && TR == 256 && D == 2, "wave layout and register ring below assume these");
   __shared__ __attribute__((aligned(16))) uint16_t sa0[TV][KC], sa1[TV][KC];
@@ -51,7 +52,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 
   int rt, vt;
   if (!map_job(blockIdx.x, nvt, nrt, split_rows, rt, vt)) return;
-  const int R = *n_ptr * K;
+  const int R = rowoff ? *n_ptr : *n_ptr * K;   // an explicit row list counts rows, not positions
   const int r0 = rt * TR;
   if (r0 >= R) return;
   const int vb = (int)((long long)vt * V / nvt);
@@ -71,6 +72,8 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     const int r = r0 + tr < R ? r0 + tr : r0;   // padding rows re-read a real row; discarded at the end
     if (xrows) {   // normalized rows, already in projected-row order
       gb[u] = (long long)r * d + piece * 8;
+    } else if (rowoff) {   // an explicit row list
+      gb[u] = rowoff[r] + piece * 8;
     } else {
       const int p = r / K, l = r - p * K;
       const int pos = rows[p];
@@ -234,7 +237,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 hipError_t launch_proj_big(const Launch& a, hipStream_t s) {
   hipLaunchKernelGGL(k_proj_bf16_big, dim3(a.plan.grid), dim3(256), 0, s, static_cast<const uint16_t*>(a.hidden),
                      static_cast<const uint16_t*>(a.w_u), a.rows, a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V,
-                     a.plan.nvt, a.plan.nrt, a.plan.split_rows, static_cast<const uint16_t*>(a.xrows),
+                     a.plan.nvt, a.plan.nrt, a.plan.split_rows, static_cast<const uint16_t*>(a.xrows), a.rowoff,
                      a.logit_scale);
   return hipGetLastError();
 }

@@ -10,12 +10,13 @@ __global__ __launch_bounds__(256) void k_proj_f32(const float* __restrict__ hidd
                                                   const int32_t* __restrict__ rows,
                                                   const int32_t* __restrict__ n_ptr, float4* __restrict__ partials,
                                                   int K, int B, int L, int d, int V, int nvt,
-                                                  const float* __restrict__ xrows, float scale) {
+                                                  const float* __restrict__ xrows,
+                                                  const long long* __restrict__ rowoff, float scale) {
   __shared__ float ws[64][33];
   __shared__ float xsm[16][33];
   __shared__ long long xoff[16];
   const int vt = blockIdx.x % nvt, rt = blockIdx.x / nvt;
-  const int R = *n_ptr * K;
+  const int R = rowoff ? *n_ptr : *n_ptr * K;   // an explicit row list counts rows, not positions
   const int r0 = rt * 16;
   if (r0 >= R) return;
   const int vb = (int)((long long)vt * V / nvt);
@@ -27,6 +28,8 @@ __global__ __launch_bounds__(256) void k_proj_f32(const float* __restrict__ hidd
     if (r < R) {
       if (xrows) {   // normalized rows, already in projected-row order
         off = (long long)r * d;
+      } else if (rowoff) {   // an explicit row list
+        off = rowoff[r];
       } else {
         const int p = r / K, l = r - p * K;
         const int pos = rows[p];
@@ -77,7 +80,7 @@ __global__ __launch_bounds__(256) void k_proj_f32(const float* __restrict__ hidd
 hipError_t launch_proj_f32(const Launch& a, hipStream_t s) {
   hipLaunchKernelGGL(k_proj_f32, dim3(a.plan.grid), dim3(256), 0, s, static_cast<const float*>(a.hidden),
                      static_cast<const float*>(a.w_u), a.rows, a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V,
-                     a.plan.nvt, static_cast<const float*>(a.xrows), a.logit_scale);
+                     a.plan.nvt, static_cast<const float*>(a.xrows), a.rowoff, a.logit_scale);
   return hipGetLastError();
 }
 

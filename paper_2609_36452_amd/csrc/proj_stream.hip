@@ -90,7 +90,8 @@ template <int NW, int MV, int NB, bool FC>
 __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
-    int nvt, int nrt, int split_rows, CompactArgs ca, const uint16_t* __restrict__ xrows, float scale) {
+    int nvt, int nrt, int split_rows, CompactArgs ca, const uint16_t* __restrict__ xrows,
+    const long long* __restrict__ rowoff, float scale) {
   constexpr int TR = 32 * NB, WR = 32 * MV, KC = 64, NT = NW * 64;
   constexpr int NLD = WR / 8;          // W_U load instructions per wave per chunk
   constexpr int XLD = TR * 8 / NT;     // hidden-row pieces per thread per chunk
@@ -140,7 +141,7 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
     R = compact_in_workgroup<NW>(ca, s_pos, TR, s_wave) * K;
     if (!has_job) return;
   } else {
-    R = *n_ptr * K;
+    R = rowoff ? *n_ptr : *n_ptr * K;   // an explicit row list counts rows, not positions
   }
   const int r0 = rt * TR;
   if (r0 >= R) return;
@@ -155,8 +156,10 @@ __global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
     xrow[u] = row;
     xpiece[u] = (q & 7) ^ ((row >> 1) & 7);
     const int r = r0 + row < R ? r0 + row : r0;
-    if (xrows) {   // normalized rows, already in projected-row order
+    if (xrows) {   // normalized rows, already in projected-row (or list) order
       xa[u] = (long long)r * d + xpiece[u] * 8;
+    } else if (rowoff) {   // an explicit row list
+      xa[u] = rowoff[r] + xpiece[u] * 8;
     } else {
       const int p = r / K, l = r - p * K;
       const int pos = FC ? s_pos[p] : rows[p];
@@ -295,12 +298,12 @@ void launch_stream(const Launch& a, hipStream_t s) {
     hipLaunchKernelGGL((k_proj_bf16_stream<NW, MV, NB, true>), dim3(p.grid), dim3(NW * 64), 0, s,
                        static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
                        a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows, ca,
-                       static_cast<const uint16_t*>(a.xrows), a.logit_scale);
+                       static_cast<const uint16_t*>(a.xrows), a.rowoff, a.logit_scale);
   else
     hipLaunchKernelGGL((k_proj_bf16_stream<NW, MV, NB, false>), dim3(p.grid), dim3(NW * 64), 0, s,
                        static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
                        a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V, p.nvt, p.nrt, p.split_rows, ca,
-                       static_cast<const uint16_t*>(a.xrows), a.logit_scale);
+                       static_cast<const uint16_t*>(a.xrows), a.rowoff, a.logit_scale);
 }
 
 }  // namespace
@@ -310,7 +313,7 @@ bool compact_fused(const Launch& a) {
   const bool streaming = v == PROJ_BF16_S32 || v == PROJ_BF16_S64 || v == PROJ_BF16_S128 || v == PROJ_BF16_S192 ||
                          v == PROJ_BF16_S256;
   return streaming && a.plan.nrt == 1 && a.max_masked > 0 && (long long)a.B * a.L <= kFusedCompactMax &&
-         !a.xrows;   // the normalization needs the row list before the projection
+         !a.xrows && !a.rowoff;   // the normalization and explicit row lists need the compaction first
 }
 
 hipError_t launch_proj_stream(const Launch& a, hipStream_t s) {

@@ -21,7 +21,7 @@ rpd_status fail(rpd_status s, const char* fmt, ...) {
   return s;
 }
 
-constexpr size_t kHeaderBytes = 256;   // n_masked, device status, completion counter
+constexpr size_t kHeaderBytes = 256;   // n_masked, device status, completion counter, lazy pass rows
 constexpr long long kMaxBL = 1LL << 24;
 constexpr int kMaxK = 64;
 
@@ -41,25 +41,29 @@ size_t partial_bytes(const rpd::ProjPlan& pl, long long rows) { return (size_t)r
 
 size_t elem_bytes(const rpd_problem* p) { return p->dtype == RPD_DTYPE_BF16 ? 2 : 4; }
 
+// per-position state of the lazy projection: act (4 B), rowoff (8 B) and
+// seven 4-byte arrays per position
+size_t lazy_bytes(long long cap) { return align256((size_t)cap * 8) + 8 * align256((size_t)cap * 4); }
+
 // the normalized, compacted rows [K * cap][d] (only with a normalization)
 size_t norm_bytes(const rpd_problem* p, long long cap) {
   return p->norm_weight ? align256((size_t)((long long)p->K * cap) * (size_t)p->d * elem_bytes(p)) : 0;
 }
 
-// Bytes for the plan chosen at `cap` masked positions; when the exact count
-// is read back later (max_masked < 0) any smaller count may be planned, so
-// the small-row variants are covered too.
+// Bytes for the plan chosen at `cap` masked positions. Any smaller row count
+// may be planned as well (the exact count read back when max_masked < 0, or
+// a lazy pass over fewer rows), so every variant boundary below it is
+// covered too.
 size_t workspace_bytes_for(const rpd_problem* p, long long cap) {
   const long long rows = (long long)p->K * cap;
   size_t part = partial_bytes(rpd::plan_projection(p->dtype, rows, p->V), rows);
-  if (p->max_masked < 0) {
-    for (long long r : {32LL, 33LL, 64LL, 65LL, 128LL, 129LL, 192LL, 193LL, 256LL, 257LL}) {
-      const long long rr = r < rows ? r : rows;
-      const size_t b = partial_bytes(rpd::plan_projection(p->dtype, rr, p->V), rr);
-      if (b > part) part = b;
-    }
+  for (long long r : {32LL, 33LL, 64LL, 65LL, 128LL, 129LL, 192LL, 193LL, 256LL, 257LL}) {
+    const long long rr = r < rows ? r : rows;
+    const size_t b = partial_bytes(rpd::plan_projection(p->dtype, rr, p->V), rr);
+    if (b > part) part = b;
   }
-  return kHeaderBytes + align256((size_t)((long long)p->B * p->L) * 4) + align256(part) + norm_bytes(p, cap);
+  return kHeaderBytes + align256((size_t)((long long)p->B * p->L) * 4) + align256(part) + lazy_bytes(cap) +
+         norm_bytes(p, cap);
 }
 
 rpd_status check_params(const rpd_params* q) {
@@ -73,7 +77,8 @@ rpd_status check_params(const rpd_params* q) {
   if (q->k_max < 1) return fail(RPD_ERR_BAD_PARAM, "k_max must be >= 1 (got %d)", q->k_max);
   if (std::isnan(q->beta) || q->beta < 0.f) return fail(RPD_ERR_BAD_PARAM, "beta must be >= 0 (got %g)", q->beta);
   if (q->window < 1) return fail(RPD_ERR_BAD_PARAM, "window must be >= 1 (got %d)", q->window);
-  if (q->flags != 0) return fail(RPD_ERR_BAD_PARAM, "flags is reserved and must be 0");
+  if (q->flags & ~(uint32_t)RPD_PARAM_LAZY)
+    return fail(RPD_ERR_BAD_PARAM, "flags holds unknown bits (0x%x); only RPD_PARAM_LAZY is defined", q->flags);
   if (q->block < 0) return fail(RPD_ERR_BAD_PARAM, "block must be >= 0 (got %d)", q->block);
   if (!std::isfinite(q->logit_scale) || q->logit_scale < 0.f)
     return fail(RPD_ERR_BAD_PARAM, "logit_scale must be finite and > 0, or 0 for 1 (got %g)", q->logit_scale);
@@ -115,6 +120,46 @@ void fill_common(rpd::Launch& a, const rpd_params* q, const rpd_outputs* o) {
   a.layer_conf = o->layer_conf;
   a.layer_entropy = o->layer_entropy;
   a.user_status = o->status;
+}
+
+// Lazy layerwise projection: one projection pass per layer from the final
+// one down over the positions still walking their agreement suffix; the
+// count of each later pass is read back (one stream synchronisation per
+// pass) to plan it, and the walk ends when it reaches zero.
+template <class Mark>
+hipError_t run_lazy(rpd::Launch& a, int dtype, hipStream_t s, Mark& mark) {
+  hipError_t e = mark(1);
+  if (e != hipSuccess) return e;
+  if (a.max_masked > 0) {
+    if ((e = rpd::launch_lazy_next(a, a.K - 1, 1, s)) != hipSuccess) return e;
+    int m_host = a.max_masked;   // pass 0 lists every projected position (<= max_masked)
+    for (int t = 0; t < a.K; ++t) {
+      const int l = a.K - 1 - t;
+      if (t > 0) {
+        int32_t m = 0;
+        if ((e = hipMemcpyAsync(&m, a.lazy.m, sizeof m, hipMemcpyDeviceToHost, s)) != hipSuccess) return e;
+        if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
+        if (m <= 0) break;
+        m_host = m;
+      }
+      rpd::Launch ap = a;
+      ap.n_masked = a.lazy.m;
+      ap.max_masked = m_host;
+      ap.rowoff = a.lazy.rowoff;
+      ap.pass_layer = l;
+      ap.fused_compact = false;
+      ap.plan = rpd::plan_projection(dtype, m_host, a.V);
+      if (ap.xrows && (e = rpd::launch_norm_rows(ap, s)) != hipSuccess) return e;
+      if ((e = rpd::launch_projection(ap, s)) != hipSuccess) return e;
+      if ((e = rpd::launch_lazy_reduce(ap, l, m_host, s)) != hipSuccess) return e;
+      if (l > 0 && (e = rpd::launch_lazy_next(a, l - 1, 0, s)) != hipSuccess) return e;
+    }
+  }
+  if ((e = mark(2)) != hipSuccess) return e;
+  if ((e = rpd::launch_lazy_score(a, s)) != hipSuccess) return e;
+  if ((e = mark(3)) != hipSuccess) return e;
+  if ((e = rpd::launch_commit(a, s)) != hipSuccess) return e;
+  return mark(4);
 }
 
 }  // namespace
@@ -191,8 +236,28 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
   a.norm_weight = p->norm_weight;
   a.norm_eps = p->norm_eps;
   a.norm_final = p->norm_final;
-  // the normalized rows sit at the end (the partials are sized for the largest plan)
+  // the normalized rows sit at the end, the lazy state before them (the
+  // partials are sized for the largest plan)
   a.xrows = p->norm_weight ? ws + (need - norm_bytes(p, cap)) : nullptr;
+  {
+    char* lz = ws + (need - norm_bytes(p, cap) - lazy_bytes(cap));
+    const size_t a4 = align256((size_t)cap * 4);
+    a.lazy.rowoff = reinterpret_cast<long long*>(lz);
+    lz += align256((size_t)cap * 8);
+    int32_t** ints[] = {&a.lazy.act, &a.lazy.y, &a.lazy.k, &a.lazy.alive, &a.lazy.depth};
+    for (int32_t** q4 : ints) {
+      *q4 = reinterpret_cast<int32_t*>(lz);
+      lz += a4;
+    }
+    float** floats[] = {&a.lazy.c, &a.lazy.h, &a.lazy.pmax};
+    for (float** q4 : floats) {
+      *q4 = reinterpret_cast<float*>(lz);
+      lz += a4;
+    }
+    a.lazy.m = reinterpret_cast<int32_t*>(ws + 12);
+  }
+  a.rowoff = nullptr;
+  const bool lazy = (q->flags & RPD_PARAM_LAZY) != 0;
   fill_common(a, q, o);
 
   auto mark = [&](int k) -> hipError_t {
@@ -204,7 +269,7 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
   a.fused_compact = false;
   if (p->max_masked >= 0) {
     a.plan = rpd::plan_projection(p->dtype, (long long)p->K * a.max_masked, p->V);
-    a.fused_compact = rpd::compact_fused(a);
+    a.fused_compact = !lazy && rpd::compact_fused(a);
   }
   hipError_t e = mark(0);
   if (e == hipSuccess && !a.fused_compact) e = rpd::launch_compact(a, s);
@@ -217,11 +282,14 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
     a.max_masked = n;
     a.plan = rpd::plan_projection(p->dtype, (long long)p->K * a.max_masked, p->V);
   }
-  if ((e = mark(1)) == hipSuccess && (!a.xrows || (e = rpd::launch_norm_rows(a, s)) == hipSuccess) &&
-      (e = rpd::launch_projection(a, s)) == hipSuccess && (e = mark(2)) == hipSuccess &&
-      (e = rpd::launch_reduce_score(a, s)) == hipSuccess && (e = mark(3)) == hipSuccess &&
-      (rpd::commit_fused(a) || (e = rpd::launch_commit(a, s)) == hipSuccess))
+  if (lazy) {
+    e = run_lazy(a, p->dtype, s, mark);
+  } else if ((e = mark(1)) == hipSuccess && (!a.xrows || (e = rpd::launch_norm_rows(a, s)) == hipSuccess) &&
+             (e = rpd::launch_projection(a, s)) == hipSuccess && (e = mark(2)) == hipSuccess &&
+             (e = rpd::launch_reduce_score(a, s)) == hipSuccess && (e = mark(3)) == hipSuccess &&
+             (rpd::commit_fused(a) || (e = rpd::launch_commit(a, s)) == hipSuccess)) {
     e = mark(4);
+  }
   if (e != hipSuccess) return fail(RPD_ERR_HIP, "launch: %s", hipGetErrorString(e));
   return RPD_OK;
 }

@@ -42,6 +42,36 @@ struct ProjPlan {
 // the shape plan for `rows_cap` rows (K * max masked positions)
 ProjPlan plan_projection(int dtype, long long rows_cap, int V);
 
+// per-position state of the lazy layerwise projection (lazy.hip)
+struct LazyState {
+  int32_t* act;        // [cap] compacted positions listed for the current pass
+  long long* rowoff;   // [cap] element offsets into hidden of their rows
+  int32_t* y;          // [cap] final-layer token
+  float* c;            // [cap] final-layer top probability
+  float* h;            // [cap] final-layer entropy
+  int32_t* k;          // [cap] agreement suffix length so far
+  float* pmax;         // [cap] peak top probability over the suffix
+  int32_t* alive;      // [cap] 1 while the walk continues
+  int32_t* depth;      // [cap] layers projected
+  int32_t* m;          // [1] rows in the current pass
+};
+
+struct LazyScoreArgs {
+  int K, B, L;
+  float theta_h, theta_c, theta_s, w;
+  int k_max;
+  int32_t* token;
+  float* entropy;
+  float* confidence;
+  int32_t* persistence;
+  float* drop;
+  float* stability;
+  uint8_t* flags;
+  int32_t* layer_argmax;
+  float* layer_conf;
+  float* layer_entropy;
+};
+
 struct Launch {
   int K, B, L, d, V;
   const void* hidden;
@@ -62,6 +92,11 @@ struct Launch {
   float norm_eps;
   int norm_final;
   void* xrows;
+  // explicit row list (lazy passes): projected row r is hidden + rowoff[r]
+  // (with K == 1 and n_masked pointing at the row count); NULL: gathered
+  const long long* rowoff;
+  int pass_layer;        // the layer of an explicit row list (normalization)
+  LazyState lazy;
   ProjPlan plan;
   // params
   float theta_h, theta_c, theta_s, w, beta;
@@ -85,6 +120,12 @@ hipError_t launch_projection(const Launch& a, hipStream_t s);
 hipError_t launch_reduce_score(const Launch& a, hipStream_t s);
 hipError_t launch_commit(const Launch& a, hipStream_t s);
 bool commit_fused(const Launch& a);
+
+// lazy layerwise projection: list the rows of layer l (first: every position),
+// reduce a pass over layer l, score from the per-position state
+hipError_t launch_lazy_next(const Launch& a, int l, int first, hipStream_t s);
+hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, hipStream_t s);
+hipError_t launch_lazy_score(const Launch& a, hipStream_t s);
 // the projection does the compaction itself (needs a.plan and a.max_masked
 // >= 0): the call then launches no compaction kernel
 bool compact_fused(const Launch& a);

@@ -60,7 +60,11 @@ _LAYER_CACHE: dict = {}
 def run_oracle(w, P: O.Params, norm=None) -> dict:
     """Oracle outputs; the per-layer projection of a workload is computed once
     per (normalization, logit scale) and reused across parameter sets. The
-    normalization epsilon is taken at float32, as the C ABI passes it."""
+    normalization epsilon is taken at float32, as the C ABI passes it. With
+    P.lazy the oracle's lazy projection runs (not cached)."""
+    if P.lazy:
+        onorm = None if norm is None else (norm[0], float(np.float32(norm[1])), bool(norm[2]))
+        return O.score_commit_lazy(w.hidden, w.w_u, w.mask, w.cfg.dtype, P, norm=onorm)
     key = (id(w), None if norm is None else id(norm[0]), norm and (norm[1], norm[2]), P.logit_scale)
     if key not in _LAYER_CACHE or _LAYER_CACHE[key][0] is not w:
         if len(_LAYER_CACHE) > 8:

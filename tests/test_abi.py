@@ -49,19 +49,24 @@ def _a256(x):
     return (x + 255) // 256 * 256
 
 
+def _lazy(cap):
+    # per-position state of the lazy projection: one 8-byte and eight 4-byte arrays
+    return _a256(cap * 8) + 8 * _a256(cap * 4)
+
+
 def test_workspace_size():
     # late-decode LLaDA shape: header + row list + (32 rows x 512 tiles of 256 vocabulary rows x 16 B)
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=8)
-    assert n == 256 + 1024 + _a256(32 * 512 * 16)
+    assert n == 256 + 1024 + _a256(32 * 512 * 16) + _lazy(8)
     # 10% masked: 104 rows x 512 tiles of 256 vocabulary rows
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=26)
-    assert n == 256 + 1024 + _a256(104 * 512 * 16)
+    assert n == 256 + 1024 + _a256(104 * 512 * 16) + _lazy(26)
     # 100% masked: 1024 rows x 494 tiles of 256 vocabulary rows
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=256)
-    assert n == 256 + 1024 + _a256(1024 * 494 * 16)
+    assert n == 256 + 1024 + _a256(1024 * 494 * 16) + _lazy(256)
     # with the final normalization: + the normalized rows (32 x 4096 bf16)
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=8, norm=True)
-    assert n == 256 + 1024 + _a256(32 * 512 * 16) + 32 * 4096 * 2
+    assert n == 256 + 1024 + _a256(32 * 512 * 16) + _lazy(8) + 32 * 4096 * 2
     assert rpd.workspace_size(0, 1, 256, 4096, 126464, rpd.DTYPE_BF16) == 0
     assert rpd.workspace_size(65, 1, 256, 4096, 126464, rpd.DTYPE_BF16) == 0
     assert rpd.workspace_size(4, 1, 256, 4096, 126464, 7) == 0
@@ -121,7 +126,7 @@ def test_problem_validation(kw, status):
 
 
 @pytest.mark.parametrize("kw", [dict(theta_c=0.95), dict(theta_c=-0.1), dict(w=-1.0), dict(k_max=0),
-                                dict(beta=-1.0), dict(beta=math.nan), dict(window=0), dict(flags=1),
+                                dict(beta=-1.0), dict(beta=math.nan), dict(window=0), dict(flags=2),
                                 dict(theta_h=math.nan), dict(theta_s=math.inf), dict(block=-1),
                                 dict(logit_scale=-1.0), dict(logit_scale=math.inf)])
 def test_param_validation(kw):

@@ -146,6 +146,36 @@ def test_fp32_normalization_and_scale():
     _check(w, O.LLADA, norm=(norm[0], 0.0, True))
 
 
+# ------------------------------------------------------- lazy projection --
+
+LAZY_CASES = [("bf16_s32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
+              ("bf16_s128", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=16, masked_frac=None), 16),
+              ("bf16_big", dict(B=1, L=120, K=4, d=200, V=6007, n_masked=100, masked_frac=None), 17)]
+
+
+@pytest.mark.parametrize("name,ov,seed", LAZY_CASES, ids=[c[0] for c in LAZY_CASES])
+def test_lazy_projection(name, ov, seed):
+    # Appendix A.6 "Layerwise projection": intermediate layers only inside the band theta_c <= c < theta_h,
+    # down to the first disagreement; decisions are the eager ones
+    base = CONFIGS["llada_late"].with_(name="lazy_" + name, **ov).with_(sharp=("calibrated",), unstable_frac=0.4)
+    w = make_workload(base, seed)
+    for P in (dataclasses.replace(O.LLADA, lazy=True), dataclasses.replace(O.DREAM, lazy=True, block=32)):
+        g, o, _ = _check(w, P)
+        eager = run_gpu(w, dataclasses.replace(P, lazy=False))
+        m = w.mask != 0
+        np.testing.assert_array_equal(g["token"][m], eager["token"][m])
+        band = m & (g["confidence"] >= P.theta_c) & (g["confidence"] < P.theta_h)
+        assert (g["persistence"][m & ~band] == -1).all() and np.isnan(g["stability"][m & ~band]).all()
+
+
+def test_lazy_projection_with_normalization_and_fp32():
+    w = make_workload(CONFIGS["tiny"].with_(sharp=("calibrated",), unstable_frac=0.4), 8)
+    _check(w, dataclasses.replace(O.LLADA, lazy=True), norm=(_gain(w, 3), 1e-6, False))
+    wb = make_workload(CONFIGS["llada_late"].with_(name="lazy_norm", B=1, L=64, K=4, d=264, V=5003, n_masked=8,
+                                                   masked_frac=None, sharp=("calibrated",), unstable_frac=0.4), 12)
+    _check(wb, dataclasses.replace(O.LLADA, lazy=True), norm=(_gain(wb, 4), 1e-5, True))
+
+
 # ------------------------------------------------------------- edge cases --
 
 def _small_bf16(seed=5, **ov):
