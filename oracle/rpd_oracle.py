@@ -27,7 +27,9 @@ Every function follows a passage of the paper (He, Liu, Xiong, Zhang,
   "RPD-block": the candidates of the active 32-position block, no budget,
   fallback to the block's most confident masked position;
 * lazy layerwise projection -- Appendix A.6 "Layerwise projection": layers
-  are projected only until a position's agreement suffix is determined.
+  are projected only until a position's agreement suffix is determined;
+* the end of an iteration (fill A_t with its predictions, keep the rest
+  masked) and a loop of iterations until the canvas is filled -- Section 3.2.
 
 Readings where the paper is silent (stated once here, used throughout):
 the supplied hidden states are already normalised (the projection is a plain
@@ -465,6 +467,33 @@ def score_commit_lazy(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dty
             o["stability"][b, i] = np.nan
     o["layers_projected"] = projected
     return o
+
+
+def apply_commit(mask: np.ndarray, canvas: np.ndarray, commit: np.ndarray, token: np.ndarray) -> None:
+    """End of an iteration (Section 3.2): every position of A_t is filled with
+    its prediction y_i and leaves the mask; the rest stay masked. In place."""
+    sel = commit != 0
+    canvas[sel] = token[sel]
+    mask[sel] = 0
+
+
+def decode_loop(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params,
+                max_iter: int | None = None) -> dict:
+    """Iterations of the commit step until no position is masked, on fixed
+    hidden states (a synthetic stand-in for the forward passes between
+    iterations): returns the canvas (-1 where never filled), the number of
+    iterations and each iteration's commit mask. The progress fallback
+    commits at least one position per iteration, so at most n iterations run."""
+    mask = mask.copy()
+    canvas = np.full(mask.shape, -1, np.int64)
+    commits = []
+    n0 = int(mask.sum())
+    limit = n0 if max_iter is None else max_iter
+    while mask.any() and len(commits) < limit:
+        o = score_commit_lazy(hidden, w_u, mask, dtype, p) if p.lazy else score_commit(hidden, w_u, mask, dtype, p)
+        commits.append(o["commit"].copy())
+        apply_commit(mask, canvas, o["commit"], o["token"])
+    return {"canvas": canvas, "iterations": len(commits), "commits": commits, "mask": mask}
 
 
 def masked_positions(mask: np.ndarray) -> list[tuple[int, int]]:

@@ -582,3 +582,38 @@ def test_lazy_projection_with_normalization():
         lazy = O.score_commit_lazy(w.hidden, w.w_u, w.mask, w.cfg.dtype, O.LLADA, norm=norm)
         for k in ("commit", "token", "flags"):
             np.testing.assert_array_equal(lazy[k], eager[k], err_msg=k)
+
+
+# ------------------------------------------------------------ decode loop ----
+# Section 3.2: A_t is filled with its predictions, the rest stay masked; the
+# fallback guarantees progress.
+
+@pytest.mark.parametrize("seed", range(4))
+def test_decode_loop_fills_the_canvas_with_each_final_argmax(seed):
+    # with the hidden states held fixed, a position's final-layer argmax never changes, so whatever the
+    # commit order the filled canvas is exactly that argmax everywhere (Eq. 1 readout, y_i)
+    w = make_workload(CONFIGS["tiny"].with_(sharp=("calibrated",)), 400 + seed)
+    P = O.Params(theta_s=2.0, w=5.0, beta=1.0)
+    r = O.decode_loop(w.hidden, w.w_u, w.mask, w.cfg.dtype, P)
+    m = w.mask != 0
+    assert not r["mask"].any()
+    pos = O.masked_positions(w.mask)
+    st = O.project_layer_stats(w.hidden, w.w_u, w.cfg.dtype, pos)
+    for a, (b, i) in enumerate(pos):
+        assert r["canvas"][b, i] == st["argmax"][a, -1]
+    assert (r["canvas"][~m] == -1).all()
+    # progress: every iteration commits at least one position, each position exactly once
+    counts = np.array([c.sum() for c in r["commits"]])
+    assert (counts >= 1).all() and counts.sum() == m.sum()
+    assert 1 <= r["iterations"] <= m.sum()
+    assert np.array_equal(np.sum(r["commits"], axis=0) != 0, m)
+
+
+def test_decode_loop_budget_orders_commitment():
+    # beta = 0 commits only candidates with no uncertain masked position before them (else the fallback):
+    # the loop then takes at least as many iterations as with a generous budget
+    w = make_workload(CONFIGS["tiny"].with_(sharp=("calibrated",)), 410)
+    tight = O.decode_loop(w.hidden, w.w_u, w.mask, w.cfg.dtype, O.Params(theta_s=2.0, w=5.0, beta=0.0))
+    loose = O.decode_loop(w.hidden, w.w_u, w.mask, w.cfg.dtype, O.Params(theta_s=2.0, w=5.0, beta=math.inf))
+    assert tight["iterations"] >= loose["iterations"]
+    np.testing.assert_array_equal(tight["canvas"], loose["canvas"])
