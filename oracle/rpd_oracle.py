@@ -471,14 +471,16 @@ def score_commit_lazy(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dty
 
 def apply_commit(mask: np.ndarray, canvas: np.ndarray, commit: np.ndarray, token: np.ndarray) -> None:
     """End of an iteration (Section 3.2): every position of A_t is filled with
-    its prediction y_i and leaves the mask; the rest stay masked. In place."""
-    sel = commit != 0
+    its prediction y_i and leaves the mask; the rest stay masked. A_t is a
+    subset of the masked positions, so a flag at a position that is no longer
+    masked changes nothing (a filled token is never overwritten). In place."""
+    sel = (mask != 0) & (commit != 0)
     canvas[sel] = token[sel]
     mask[sel] = 0
 
 
 def decode_loop(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params,
-                max_iter: int | None = None) -> dict:
+                max_iter: int | None = None, norm: tuple | None = None) -> dict:
     """Iterations of the commit step until no position is masked, on fixed
     hidden states (a synthetic stand-in for the forward passes between
     iterations): returns the canvas (-1 where never filled), the number of
@@ -490,7 +492,7 @@ def decode_loop(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: st
     n0 = int(mask.sum())
     limit = n0 if max_iter is None else max_iter
     while mask.any() and len(commits) < limit:
-        o = score_commit_lazy(hidden, w_u, mask, dtype, p) if p.lazy else score_commit(hidden, w_u, mask, dtype, p)
+        o = (score_commit_lazy if p.lazy else score_commit)(hidden, w_u, mask, dtype, p, norm=norm)
         commits.append(o["commit"].copy())
         apply_commit(mask, canvas, o["commit"], o["token"])
     return {"canvas": canvas, "iterations": len(commits), "commits": commits, "mask": mask}

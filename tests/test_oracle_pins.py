@@ -617,3 +617,15 @@ def test_decode_loop_budget_orders_commitment():
     loose = O.decode_loop(w.hidden, w.w_u, w.mask, w.cfg.dtype, O.Params(theta_s=2.0, w=5.0, beta=math.inf))
     assert tight["iterations"] >= loose["iterations"]
     np.testing.assert_array_equal(tight["canvas"], loose["canvas"])
+
+
+def test_apply_commit_fills_only_masked_positions():
+    # A_t is drawn from the masked positions (Section 3.2): a flag where the canvas is already filled,
+    # or was never masked, leaves both the token and the mask as they are
+    mask = np.array([[1, 1, 0, 1, 0]], np.uint8)
+    canvas = np.array([[-1, -1, 7, -1, 9]], np.int64)
+    O.apply_commit(mask, canvas, np.array([[1, 0, 1, 1, 1]], np.uint8), np.array([[10, 11, 12, 13, 14]]))
+    assert mask.tolist() == [[0, 1, 0, 0, 0]] and canvas.tolist() == [[10, -1, 7, 13, 9]]
+    # a second iteration flagging the same positions again changes nothing there
+    O.apply_commit(mask, canvas, np.array([[1, 1, 0, 1, 0]], np.uint8), np.array([[20, 21, 22, 23, 24]]))
+    assert mask.tolist() == [[0, 0, 0, 0, 0]] and canvas.tolist() == [[10, 21, 7, 13, 9]]
