@@ -123,12 +123,149 @@ def cpu_baseline(w, P, budget_s: float) -> dict:
                       f"V={w.cfg.V}, d={w.cfg.d}) in float64, {t:.1f} s"}
 
 
+def proj_cost(cfg, rows: int):
+    """Algorithmic HBM bytes and flops of one projection launch over ``rows``
+    rows: W_U read once plus the rows, 2 flops per multiply-add."""
+    el = 2 if cfg.dtype == "bf16" else 4
+    return cfg.V * cfg.d * el + rows * cfg.d * el, 2.0 * rows * cfg.V * cfg.d
+
+
+def decode_cpu_baseline(w, P, counts: list, budget_s: float) -> dict:
+    """The oracle on the host: one whole call of the step on the fully masked
+    first iteration, timed while it fits the budget, then scaled to a whole
+    decode by the masked counts of the decode's iterations (the oracle's cost
+    is proportional to the masked positions it projects)."""
+    import oracle as O
+    t, reps = 0.0, 0
+    while reps == 0 or (t * (reps + 1) / reps < budget_s and reps < 64):
+        t0 = time.perf_counter()
+        pos, layer = O.layer_stats_masked(w.hidden, w.w_u, w.mask, w.cfg.dtype)
+        O.assemble(w.mask, pos, layer, P)
+        t += time.perf_counter() - t0
+        reps += 1
+    per_pos = t / reps / w.n_masked
+    est = per_pos * sum(counts)
+    return {"value": w.n_masked / est, "unit": "positions/s", "cores": blas_threads(), "kind": "oracle",
+            "sample": f"{reps} whole call(s) of the step at the first iteration ({w.n_masked} masked positions x "
+                      f"{w.cfg.K} layers, V={w.cfg.V}, d={w.cfg.d}) in float64, {t:.1f} s; scaled to the "
+                      f"{sum(counts)} position-iterations of the decode"}
+
+
+def bench_decode(args, w, P, hidden, w_u, mask, norm_kw) -> int:
+    """Whole decodes: iterations of score-commit + canvas update until no
+    position is masked, each decode from the same initial mask, HIP-graph
+    replays with a read-back of the masked count every --sync-every
+    iterations (the host has to learn when to stop)."""
+    import numpy as np
+    import torch
+    from paper_2609_36452_amd import binding as rpd
+    cfg = w.cfg
+    dec = rpd.Decoder(hidden, w_u, mask, P, graph=not P.lazy, sync_every=args.sync_every, **norm_kw)
+    log(f"decode warmup {args.warmup} (first decode captures the plans)")
+    r = None
+    for _ in range(max(args.warmup, 1)):
+        dec.reset()
+        r = dec.run()
+    torch.cuda.synchronize()
+    nfe, calls = r["iterations"], r["calls"]
+    log(f"  NFE {nfe}, calls per decode {calls}, graphs captured {dec.captures}")
+    K = args.steps
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"timing {K} decodes")
+    t_wall0 = time.perf_counter()
+    start.record()
+    for _ in range(K):
+        dec.reset()
+        r = dec.run()
+    end.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall0
+    ms_dec = start.elapsed_time(end) / K
+    assert r["iterations"] == nfe
+    # the same decode eagerly (launch by launch), for the launch overhead the graphs remove
+    eager = rpd.Decoder(hidden, w_u, mask, P, graph=False, sync_every=args.sync_every, **norm_kw)
+    eager.run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ke = max(1, min(K, 5))
+    e0.record()
+    for _ in range(ke):
+        eager.reset()
+        eager.run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_eager = e0.elapsed_time(e1) / ke
+    # projection time per iteration (stage events; eager)
+    timed = rpd.Decoder(hidden, w_u, mask, P, graph=False, sync_every=args.sync_every, **norm_kw)
+    rt = timed.run(stage_events=True)
+    counts = [w.n_masked] + rt["left"][:-1]
+    proj = rt["proj_ms"][:len(counts)]
+    cls = {"hbm": [0.0, 0.0], "mfma": [0.0, 0.0]}
+    sol = 0.0
+    for n, ms in zip(counts, proj):
+        by, fl = proj_cost(cfg, n * cfg.K)
+        c = "hbm" if n * cfg.K < RIDGE_ROWS else "mfma"
+        cls[c][0] += by if c == "hbm" else fl
+        cls[c][1] += ms
+        sol += max(by / (HBM_PEAK_GBS * 1e9), fl / (MFMA_BF16_PEAK_TFLOPS * 1e12)) * 1e3
+    dom = max(cls, key=lambda c: cls[c][1])
+    amount, ms_sum = cls[dom]
+    if dom == "hbm":
+        ach = amount / (ms_sum / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4)}
+    else:
+        ach = amount / (ms_sum / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4)}
+    roof["traffic"] = None
+    roof["kernel"] = f"projection launches of the {dom}-bound iterations (varying variant)"
+    roof["iterations"] = sum(1 for n in counts if (n * cfg.K < RIDGE_ROWS) == (dom == "hbm"))
+    roof["kernel_ms_per_decode"] = round(ms_sum, 4)
+    roof["projection_ms_per_decode"] = round(float(np.sum(proj)), 4)
+    roof["speed_of_light_frac"] = round(sol / float(np.sum(proj)), 4)
+    value = w.n_masked / (ms_dec / 1e3)
+    log(f"  {ms_dec:.3f} ms/decode (eager {ms_eager:.3f}), {nfe / ms_dec * 1e3:.0f} iterations/s, wall {t_wall:.2f} s")
+    out = {
+        "metric": "positions decoded/sec over whole decodes at LLaDA-8B shape (score-commit + canvas update "
+                  "per iteration until no mask)",
+        "value": round(value, 1),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_dec, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded random W_U ~ N(0,1/d) and hidden states of the model shape, held fixed "
+                "between iterations)",
+        "config": {"workload": f"{cfg.name} decode: d={cfg.d} V={cfg.V} B={cfg.B} L={cfg.L} K={cfg.K} "
+                               f"{w.n_masked} masked at the start, rule={args.rule} beta={P.beta}"
+                               + (f" block={P.block}" if P.block else ""),
+                   "nfe": nfe, "calls_per_decode": calls, "sync_every": args.sync_every,
+                   "graphs": dec.captures, "commit_rule": "rpd_block" if P.block else "rpd",
+                   "final_norm": bool(args.norm), "lazy_projection": bool(P.lazy)},
+        "iterations_per_s": round(nfe / ms_dec * 1e3, 1),
+        "eager_ms_per_step": round(ms_eager, 5),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline and not args.norm:
+        import oracle as O
+        log("cpu baseline (oracle)")
+        out["cpu_baseline"] = decode_cpu_baseline(w, O.Params(**P.__dict__), counts, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="llada_late")
+    ap.add_argument("--config", default=None,
+                    help="workload (default llada_late; llada_100, a fully masked canvas, with --decode)")
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--rule", default="strict", choices=["strict", "llada", "dream", "llada_block"],
                     help="commit rule: strict agreement (default), the paper's LLaDA / Dream settings, or "
@@ -142,7 +279,14 @@ def main() -> int:
                     help="pass a normalization gain: layers 0..K-2 go through the final normalization first")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain copy kernel of known size (for scaling HBM byte counters)")
+    ap.add_argument("--decode", action="store_true",
+                    help="time whole decodes instead of single calls: score-commit and canvas update per "
+                         "iteration until no position is masked (HIP-graph replays)")
+    ap.add_argument("--sync-every", type=int, default=8,
+                    help="--decode: iterations between read-backs of the masked count")
     args = ap.parse_args()
+    if args.config is None:
+        args.config = "llada_100" if args.decode else "llada_late"
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the commit step is benchmarked on a single MI355X "
               f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
@@ -187,6 +331,8 @@ def main() -> int:
         gt = torch.from_numpy(round_bf16_bits(g)).view(torch.bfloat16) if cfg.dtype == "bf16" else \
             torch.from_numpy(g.astype(np.float32))
         norm_kw = dict(norm_weight=gt.to(dev), norm_eps=1e-5)
+    if args.decode:
+        return bench_decode(args, w, P, hidden, w_u, mask, norm_kw)
     call = rpd.ScoreCommit(hidden, w_u, mask, P, max_masked=w.n_masked, **norm_kw)
     variant = rpd.projection_variant(cfg.K, cfg.B, cfg.L, cfg.d, cfg.V, hidden.dtype, max_masked=w.n_masked)
     log(f"projection variant {variant}")

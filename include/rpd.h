@@ -270,6 +270,34 @@ enum {
  */
 int32_t rpd_projection_variant(const rpd_problem* p);
 
+/*
+ * The end of an iteration (Section 3.2: the positions of A_t are filled with
+ * their predictions y_i; every other position keeps its mask): for every
+ * masked position with commit != 0, canvas = token and mask = 0.
+ *   mask     [B][L] uint8, updated in place
+ *   canvas   [B][L] int32, written only at the positions committed here
+ *   commit, token  [B][L] uint8 / int32 as rpd_score_commit writes them
+ *   progress optional int32 [1 + progress_len], zeroed by the caller before
+ *            the first call: progress[0] counts the calls made with it and
+ *            progress[1 + t] receives the number of positions still masked
+ *            after call t (for t < progress_len), so a loop of iterations
+ *            learns when the canvas is full without a read-back per
+ *            iteration. With it the update runs in one workgroup (meant for
+ *            canvases of up to some tens of thousands of positions); without
+ *            it, over the whole GPU.
+ *   step     optional int32 [B][L] (needs progress): at each position
+ *            committed here, the call index progress[0] had on entry.
+ * All pointers are device memory owned by the caller. NULL mask, canvas,
+ * commit or token, or step without progress, -> RPD_ERR_NULL_POINTER; B or L
+ * < 1 or B*L > 2^24 -> RPD_ERR_BAD_SHAPE; progress_len < 0 ->
+ * RPD_ERR_BAD_PARAM. Enqueued on `stream`; it allocates nothing and never
+ * synchronises, so a loop body of rpd_score_commit (max_masked >= 0, lazy
+ * projection off) followed by this call can be captured in a HIP graph.
+ */
+rpd_status rpd_apply_commit(int32_t B, int32_t L, uint8_t* mask, int32_t* canvas, const uint8_t* commit,
+                            const int32_t* token, int32_t* progress, int32_t progress_len, int32_t* step,
+                            void* stream);
+
 /* Static text for a status code. */
 const char* rpd_status_string(rpd_status s);
 

@@ -118,6 +118,10 @@ def lib() -> ctypes.CDLL:
         L.rpd_gate_commit.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.POINTER(RpdParams), ctypes.POINTER(RpdOutputs), ctypes.c_void_p]
+        L.rpd_apply_commit.restype = ctypes.c_int
+        L.rpd_apply_commit.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                       ctypes.c_void_p, ctypes.c_void_p]
         L.rpd_status_string.restype = ctypes.c_char_p
         L.rpd_status_string.argtypes = [ctypes.c_int]
         L.rpd_last_error.restype = ctypes.c_char_p
@@ -306,3 +310,138 @@ def gate_commit(mask: torch.Tensor, layer_argmax: torch.Tensor, layer_conf: torc
                                  layer_conf.data_ptr(), layer_entropy.data_ptr(), ctypes.byref(q),
                                  ctypes.byref(oc), _stream_handle(stream)))
     return out
+
+
+def apply_commit(mask: torch.Tensor, canvas: torch.Tensor, commit: torch.Tensor, token: torch.Tensor,
+                 progress: torch.Tensor | None = None, step: torch.Tensor | None = None, stream=None) -> None:
+    """``rpd_apply_commit``: committed positions take their token in the
+    canvas and leave the mask (in place). mask [B][L] uint8/bool, canvas and
+    token [B][L] int32, commit [B][L] uint8; optional progress int32
+    [1 + n] (call counter, then the masked count left after each call) and
+    step int32 [B][L] (the call index at which each position was filled)."""
+    B, L = mask.shape
+    _check_dev("mask", mask, (B, L), (torch.uint8, torch.bool))
+    _check_dev("canvas", canvas, (B, L), (torch.int32,))
+    _check_dev("commit", commit, (B, L), (torch.uint8,))
+    _check_dev("token", token, (B, L), (torch.int32,))
+    n = 0
+    if progress is not None:
+        if progress.dim() != 1 or progress.numel() < 1:
+            raise ValueError("progress must be a 1-d tensor of at least one element")
+        _check_dev("progress", progress, (progress.numel(),), (torch.int32,))
+        n = progress.numel() - 1
+    if step is not None:
+        _check_dev("step", step, (B, L), (torch.int32,))
+    _check(lib().rpd_apply_commit(B, L, mask.view(torch.uint8).data_ptr(), canvas.data_ptr(), commit.data_ptr(),
+                                  token.data_ptr(), _ptr(progress), n, _ptr(step), _stream_handle(stream)))
+
+
+class Decoder:
+    """Iterations of the commit step until no position is masked (Section
+    3.2): each iteration is ``rpd_score_commit`` followed by
+    ``rpd_apply_commit`` on the same stream, over hidden states that stay
+    fixed between iterations (they stand in for the forward passes of the
+    model, which this library does not run).
+
+    Every iteration commits at least one masked position (the progress
+    fallback), so after t iterations at most n0 - t positions are masked; that
+    bound is the ``max_masked`` of the call, and the masked count left after
+    each iteration is recorded on the device (``progress``) and read back
+    only every ``sync_every`` iterations, to tighten the bound and to stop.
+    Iterations that find the canvas already full change nothing. With
+    ``graph=True`` one iteration is captured in a HIP graph per plan and
+    replayed: a plan is made for the first bound that needs it and serves
+    every smaller bound of the same projection variant (down to half its
+    bound for the variants whose grid grows with the rows). Plans are kept
+    across ``reset()``, so repeated decodes replay the same graphs. Lazy
+    projection reads counts back inside the call, so it always runs
+    eagerly."""
+
+    def __init__(self, hidden: torch.Tensor, w_u: torch.Tensor, mask: torch.Tensor, params: Params,
+                 norm_weight: torch.Tensor | None = None, norm_eps: float = 1e-5, norm_final: bool = False,
+                 graph: bool = True, sync_every: int = 8):
+        K, B, L, d = hidden.shape
+        _check_dev("mask", mask, (B, L), (torch.uint8, torch.bool))
+        self.hidden, self.w_u, self.params = hidden, w_u, params
+        self.norm = dict(norm_weight=norm_weight, norm_eps=norm_eps, norm_final=norm_final)
+        self.graph = bool(graph) and not params.lazy
+        self.sync_every = max(1, int(sync_every))
+        self.shape = (K, B, L, d, w_u.shape[0])
+        dev = hidden.device
+        self.mask0 = mask.view(torch.uint8).clone()
+        self.mask = self.mask0.clone()
+        self.n0 = int(self.mask0.sum().item())
+        self.canvas = torch.full((B, L), -1, dtype=torch.int32, device=dev)
+        self.step = torch.full((B, L), -1, dtype=torch.int32, device=dev)
+        self.progress = torch.zeros(1 + max(self.n0, 1), dtype=torch.int32, device=dev)
+        self._plans: dict[str, list] = {}   # variant -> [(bound, ScoreCommit, graph or None)]
+        self.captures = 0
+        self.bounds: list[int] = []    # the max_masked of each enqueued iteration
+
+    def reset(self) -> None:
+        """Start a new decode from the initial mask (the plans are kept)."""
+        self.mask.copy_(self.mask0)
+        self.canvas.fill_(-1)
+        self.step.fill_(-1)
+        self.progress.zero_()
+        self.bounds = []
+
+    def _iteration(self, sc: ScoreCommit, events=None) -> None:
+        o = sc(events=events)
+        apply_commit(self.mask, self.canvas, o["commit"], o["token"], self.progress, self.step)
+
+    def _plan_for(self, bound: int):
+        K, B, L, d, V = self.shape
+        variant = projection_variant(K, B, L, d, V, self.hidden.dtype, max_masked=bound)
+        plans = self._plans.setdefault(variant, [])
+        fits = [p for p in plans if p[0] >= bound and (variant.startswith("bf16_s") or 2 * bound > p[0])]
+        if fits:
+            return min(fits, key=lambda p: p[0])
+        sc = ScoreCommit(self.hidden, self.w_u, self.mask, self.params, max_masked=bound, **self.norm)
+        g = None
+        if self.graph:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                self._iteration(sc)
+            self.captures += 1
+        plans.append((bound, sc, g))
+        return plans[-1]
+
+    def run(self, max_iter: int | None = None, stage_events: bool = False) -> dict:
+        """Decode until the canvas is full (or ``max_iter`` iterations);
+        returns the canvas (-1 where never filled), the iteration at which
+        each position was filled (``step``, -1 if never), the number of
+        iterations that committed something (``iterations``, the NFE of the
+        loop), the masked count left after each of them (``left``) and the
+        number of enqueued iterations (``calls``). With ``stage_events``
+        every iteration runs eagerly with events around its projection stage
+        and ``proj_ms`` lists the projection time of each iteration."""
+        limit = self.n0 if max_iter is None else min(int(max_iter), self.n0)
+        t, known, t_known = 0, self.n0, 0
+        ev = []
+        while t < limit and known > 0:
+            chunk = min(self.sync_every, limit - t)
+            for _ in range(chunk):
+                bound = max(known - (t - t_known), 1)
+                bnd, sc, g = self._plan_for(bound)
+                self.bounds.append(bnd)
+                if stage_events:
+                    pair = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                    for e in pair:         # torch creates the HIP event at its first record
+                        e.record()
+                    ev.append(pair)
+                    self._iteration(sc, events=[None, pair[0], pair[1]])
+                elif g is not None:
+                    g.replay()
+                else:
+                    self._iteration(sc)
+                t += 1
+            known, t_known = int(self.progress[t].item()), t
+        left = self.progress[1:1 + t].cpu().tolist()
+        iters = next((i + 1 for i, n in enumerate(left) if n == 0), t)
+        out = {"canvas": self.canvas, "step": self.step, "mask": self.mask, "iterations": iters,
+               "left": left[:iters], "calls": t}
+        if stage_events:
+            torch.cuda.synchronize()
+            out["proj_ms"] = [a.elapsed_time(b) for a, b in ev]
+        return out

@@ -305,6 +305,21 @@ rpd_status rpd_score_commit_timed(const rpd_problem* p, const rpd_params* q, con
   return score_commit_impl(p, q, o, workspace, workspace_bytes, stream, events, n_events);
 }
 
+rpd_status rpd_apply_commit(int32_t B, int32_t L, uint8_t* mask, int32_t* canvas, const uint8_t* commit,
+                            const int32_t* token, int32_t* progress, int32_t progress_len, int32_t* step,
+                            void* stream) {
+  g_err[0] = '\0';
+  if (!mask || !canvas || !commit || !token) return fail(RPD_ERR_NULL_POINTER, "mask, canvas, commit and token are required");
+  if (step && !progress) return fail(RPD_ERR_NULL_POINTER, "step needs progress (the call counter)");
+  if (B < 1 || L < 1 || (long long)B * L > kMaxBL)
+    return fail(RPD_ERR_BAD_SHAPE, "need B,L>=1, B*L<=2^24 (got B=%d L=%d)", B, L);
+  if (progress && progress_len < 0) return fail(RPD_ERR_BAD_PARAM, "progress_len must be >= 0");
+  const hipError_t e = rpd::launch_apply_commit((long long)B * L, mask, canvas, commit, token, progress,
+                                                progress ? progress_len : 0, step, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(RPD_ERR_HIP, "launch: %s", hipGetErrorString(e));
+  return RPD_OK;
+}
+
 rpd_status rpd_gate_commit(int32_t K, int32_t B, int32_t L, const uint8_t* mask, const int32_t* layer_argmax,
                            const float* layer_conf, const float* layer_entropy, const rpd_params* q,
                            const rpd_outputs* o, void* stream) {

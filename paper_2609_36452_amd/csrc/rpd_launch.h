@@ -137,6 +137,11 @@ hipError_t launch_proj_stream(const Launch& a, hipStream_t s);  // PROJ_BF16_S32
 hipError_t launch_proj_big(const Launch& a, hipStream_t s);     // PROJ_BF16_BIG
 hipError_t launch_proj_f32(const Launch& a, hipStream_t s);     // PROJ_F32
 
+// end of an iteration: fill the canvas with the committed tokens, unmask them
+hipError_t launch_apply_commit(long long BL, uint8_t* mask, int32_t* canvas, const uint8_t* commit,
+                               const int32_t* token, int32_t* progress, int progress_len, int32_t* step,
+                               hipStream_t s);
+
 // scoring + commitment from caller-supplied per-layer statistics
 hipError_t launch_gate_commit(const Launch& a, const int32_t* layer_argmax, const float* layer_conf,
                               const float* layer_entropy, hipStream_t s);

@@ -1,6 +1,8 @@
 // K0 masked-position compaction, K2 cross-tile reduction with the
 // layerwise stability test (Eq. 2-5), K3 budgeted commitment with the
 // progress fallback (Section 3.2), and their launchers.
+#include <algorithm>
+
 #include "rpd_device.h"
 
 namespace rpd {
@@ -455,6 +457,46 @@ __global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4
   commit_sequence(mask, ca, 0, GlobalScores{ca.flags, ca.entropy, ca.confidence});
 }
 
+// End of an iteration (Section 3.2): committed positions take their token in
+// the canvas and leave the mask. With `progress`, one workgroup does the
+// whole canvas and records the masked positions left: progress[0] counts the
+// calls, progress[1 + t] holds call t's remainder (while t < progress_len),
+// and `step` (optional) receives the call index at each committed position.
+// Without it the canvas is covered grid-stride.
+constexpr int kApplyThreads = 1024;
+__global__ __launch_bounds__(kApplyThreads) void k_apply_commit(long long BL, uint8_t* __restrict__ mask,
+                                                                int32_t* __restrict__ canvas,
+                                                                const uint8_t* __restrict__ commit,
+                                                                const int32_t* __restrict__ token,
+                                                                int32_t* __restrict__ progress, int progress_len,
+                                                                int32_t* __restrict__ step) {
+  __shared__ int wsum[kApplyThreads / 64];
+  const int t = progress ? progress[0] : 0;
+  int left = 0;
+  for (long long o = blockIdx.x * (long long)blockDim.x + threadIdx.x; o < BL; o += (long long)gridDim.x * blockDim.x) {
+    if (mask[o] != 0) {
+      if (commit[o] != 0) {
+        canvas[o] = token[o];
+        mask[o] = 0;
+        if (step) step[o] = t;
+      } else {
+        ++left;
+      }
+    }
+  }
+  if (!progress) return;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) left += __shfl_xor(left, m);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = left;
+  __syncthreads();   // also orders every thread's read of progress[0] before its update
+  if (threadIdx.x == 0) {
+    int tot = 0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) tot += wsum[w];
+    if (t < progress_len) progress[1 + t] = tot;
+    progress[0] = t + 1;
+  }
+}
+
 ScoreArgs score_args(const Launch& a) {
   ScoreArgs s;
   s.K = a.K;
@@ -526,6 +568,15 @@ int commit_threads(int L) {
 
 hipError_t launch_commit(const Launch& a, hipStream_t s) {
   hipLaunchKernelGGL(k_commit, dim3(a.B), dim3(commit_threads(a.L)), 0, s, a.mask, commit_args(a));
+  return hipGetLastError();
+}
+
+hipError_t launch_apply_commit(long long BL, uint8_t* mask, int32_t* canvas, const uint8_t* commit,
+                               const int32_t* token, int32_t* progress, int progress_len, int32_t* step,
+                               hipStream_t s) {
+  const unsigned grid = progress ? 1u : (unsigned)std::min<long long>((BL + kApplyThreads - 1) / kApplyThreads, 1024);
+  hipLaunchKernelGGL(k_apply_commit, dim3(grid), dim3(kApplyThreads), 0, s, BL, mask, canvas, commit, token, progress,
+                     progress_len, step);
   return hipGetLastError();
 }
 

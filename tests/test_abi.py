@@ -158,3 +158,15 @@ def test_gate_validation():
     assert L.rpd_gate_commit(0, 1, 16, 64, 64, 64, 64, ctypes.byref(q), ctypes.byref(o), None) == 2
     bad = _params(beta=-2.0)
     assert L.rpd_gate_commit(4, 1, 16, 64, 64, 64, 64, ctypes.byref(bad), ctypes.byref(o), None) == 3
+
+
+def test_apply_commit_validation():
+    L = rpd.lib()
+    # (B, L, mask, canvas, commit, token, progress, progress_len, step, stream); nothing is launched
+    assert L.rpd_apply_commit(1, 16, None, 64, 64, 64, None, 0, None, None) == 1
+    assert L.rpd_apply_commit(1, 16, 64, 64, 64, None, None, 0, None, None) == 1
+    assert L.rpd_apply_commit(1, 16, 64, 64, 64, 64, None, 0, 64, None) == 1      # step needs progress
+    assert L.rpd_apply_commit(0, 16, 64, 64, 64, 64, None, 0, None, None) == 2
+    assert L.rpd_apply_commit(1 << 13, 1 << 12, 64, 64, 64, 64, None, 0, None, None) == 2
+    assert L.rpd_apply_commit(1, 16, 64, 64, 64, 64, 64, -1, None, None) == 3
+    assert "progress" in rpd.last_error()

@@ -1,0 +1,222 @@
+"""The decode loop on the GPU (Section 3.2): rpd_score_commit followed by
+rpd_apply_commit, iterated until the canvas is full, eagerly and as HIP-graph
+replays, against the oracle.
+
+Each iteration is checked to the parity bar of the single call (the oracle
+evaluated on the GPU's own mask of that iteration), and the whole trajectory
+-- the canvas, the iteration at which each position was filled, the masked
+count after each iteration -- must equal the lockstep run of the same calls.
+Where no commitment or token decision of the run was a near-tie, the
+trajectory must also equal the oracle's own decode loop."""
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from gpu_util import gain_tensor, gpu_params, note, to_device
+from paper_2609_36452_amd import binding as rpd
+from paper_2609_36452_amd.workload import CONFIGS, make_workload, round_bf16_bits
+from parity import compare
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _np(t):
+    return t.cpu().numpy()
+
+
+# ----------------------------------------------------------- apply_commit --
+
+@pytest.mark.parametrize("B,L", [(1, 1), (3, 1000), (2, 4099)])
+def test_apply_commit_matches_oracle(B, L):
+    g = np.random.default_rng(B * 7919 + L)
+    mask = (g.random((B, L)) < 0.7).astype(np.uint8)
+    canvas = np.full((B, L), -1, np.int64)
+    step = np.full((B, L), -1, np.int64)
+    dm = torch.from_numpy(mask).to(DEV)
+    dc = torch.full((B, L), -1, dtype=torch.int32, device=DEV)
+    ds = torch.full((B, L), -1, dtype=torch.int32, device=DEV)
+    prog = torch.zeros(1 + 3, dtype=torch.int32, device=DEV)
+    left = []
+    for t in range(4):          # one call past progress_len: the count of calls still advances
+        commit = (g.random((B, L)) < 0.3).astype(np.uint8)
+        token = g.integers(0, 1 << 20, (B, L)).astype(np.int32)
+        note(f"  apply_commit B={B} L={L} call {t}")
+        rpd.apply_commit(dm, dc, torch.from_numpy(commit).to(DEV), torch.from_numpy(token).to(DEV), prog, ds)
+        sel = (mask != 0) & (commit != 0)
+        step[sel] = t
+        O.apply_commit(mask, canvas, commit, token)
+        left.append(int(mask.sum()))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(_np(dm), mask)
+    np.testing.assert_array_equal(_np(dc), canvas)
+    np.testing.assert_array_equal(_np(ds), step)
+    assert _np(prog).tolist() == [4] + left[:3]
+
+
+def test_apply_commit_grid_stride():
+    # without progress the update covers the canvas grid-stride (2^20 positions)
+    B, L = 64, 1 << 14
+    g = np.random.default_rng(5)
+    mask = (g.random((B, L)) < 0.5).astype(np.uint8)
+    commit = (g.random((B, L)) < 0.5).astype(np.uint8)
+    token = g.integers(0, 126464, (B, L)).astype(np.int32)
+    canvas = np.full((B, L), -1, np.int64)
+    dm, dc = torch.from_numpy(mask).to(DEV), torch.full((B, L), -1, dtype=torch.int32, device=DEV)
+    note(f"  apply_commit grid-stride B={B} L={L}")
+    rpd.apply_commit(dm, dc, torch.from_numpy(commit).to(DEV), torch.from_numpy(token).to(DEV))
+    O.apply_commit(mask, canvas, commit, token)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(_np(dm), mask)
+    np.testing.assert_array_equal(_np(dc), canvas)
+
+
+# ------------------------------------------------------------ decode loop --
+
+def _lockstep(w, P, bounds, tensors, norm=None):
+    """The GPU calls of a decode at the given max_masked bounds, each compared
+    with the oracle on the GPU's mask of that iteration. Returns the
+    trajectory and whether any commitment or token decision differed from the
+    oracle's (allowed only where the parity contract excuses it)."""
+    hidden, w_u, mask0 = tensors
+    onorm = None if norm is None else (norm[0], float(np.float32(norm[1])), bool(norm[2]))
+    pos, layer = O.layer_stats_masked(w.hidden, w.w_u, w.mask, w.cfg.dtype, norm=onorm, logit_scale=P.logit_scale)
+    index = {p: a for a, p in enumerate(pos)}
+    kw = {}
+    if norm is not None:
+        kw = dict(norm_weight=gain_tensor(w, norm[0], hidden.device), norm_eps=norm[1], norm_final=norm[2])
+    B, L = w.mask.shape
+    mask = mask0.clone()
+    canvas = torch.full((B, L), -1, dtype=torch.int32, device=DEV)
+    step = torch.full((B, L), -1, dtype=torch.int32, device=DEV)
+    prog = torch.zeros(1 + len(bounds), dtype=torch.int32, device=DEV)
+    diverged = False
+    for t, bound in enumerate(bounds):
+        m = _np(mask)
+        pos_t = O.masked_positions(m)
+        sub = {k: v[[index[p] for p in pos_t]] for k, v in layer.items()}
+        o = O.assemble(m, pos_t, sub, P)
+        g = rpd.score_commit(hidden, w_u, mask, gpu_params(P), max_masked=bound, layer_stats=True, **kw)
+        torch.cuda.synchronize()
+        gn = {k: _np(v) for k, v in g.items()}
+        rep = compare(gn, o, m, P, w.cfg.d)
+        assert rep.ok(), f"iteration {t} (bound {bound}): " + rep.summary()
+        mm = m != 0
+        if (gn["commit"][mm] != o["commit"][mm]).any() or (gn["token"][mm] != o["token"][mm]).any():
+            diverged = True
+        rpd.apply_commit(mask, canvas, g["commit"], g["token"], prog, step)
+    torch.cuda.synchronize()
+    return {"canvas": _np(canvas), "step": _np(step), "left": _np(prog)[1:].tolist(), "diverged": diverged}
+
+
+def _oracle_steps(od, shape):
+    st = np.full(shape, -1, np.int64)
+    for t, c in enumerate(od["commits"]):
+        st[c != 0] = t
+    return st
+
+
+DECODE_CASES = [
+    # name, workload overrides, seed, params; the bf16 canvases start fully masked so the bound falls
+    # through the big-tile and every streaming variant
+    ("tiny_f32", "tiny", dict(sharp=("ushape", 12.0)), 3, O.LLADA),
+    ("bf16_two_seqs", "llada_late", dict(name="dec2", B=2, L=64, K=4, d=264, V=3001, n_masked=None,
+                                         masked_frac=1.0, sharp=("ushape", 12.0), unstable_frac=0.3), 5,
+     O.LLADA),
+    ("bf16_calibrated_strict", "llada_late", dict(name="dec3", B=1, L=96, K=4, d=200, V=2503, n_masked=None,
+                                                  masked_frac=0.8, sharp=("calibrated",), unstable_frac=0.3), 6,
+     O.strict(4, 1.0)),
+    ("bf16_rpd_block", "llada_late", dict(name="dec4", B=1, L=96, K=4, d=200, V=2503, n_masked=None,
+                                          masked_frac=1.0, sharp=("ushape", 12.0), unstable_frac=0.3), 7,
+     O.Params(theta_s=3.5, w=15.0, block=32)),
+]
+
+
+@pytest.mark.parametrize("graph", [True, False], ids=["graph", "eager"])
+@pytest.mark.parametrize("name,base,ov,seed,P", DECODE_CASES, ids=[c[0] for c in DECODE_CASES])
+def test_decode_loop(name, base, ov, seed, P, graph):
+    w = make_workload(CONFIGS[base].with_(**ov), seed)
+    tensors = to_device(w)
+    note(f"  decode {name} n={w.n_masked} graph={graph}")
+    dec = rpd.Decoder(*tensors, gpu_params(P), graph=graph, sync_every=5)
+    r = dec.run()
+    torch.cuda.synchronize()
+    n_it = r["iterations"]
+    note(f"    iterations {n_it}, calls {r['calls']}, captures {dec.captures}, bounds {dec.bounds[:n_it]}")
+    assert not _np(r["mask"]).any()
+    assert r["left"][-1] == 0 and all(a > b for a, b in zip([w.n_masked] + r["left"], r["left"]))
+    assert r["calls"] >= n_it and len(dec.bounds) == r["calls"]
+    if graph:
+        assert 1 <= dec.captures < r["calls"]
+    ls = _lockstep(w, P, dec.bounds[:n_it], tensors)
+    np.testing.assert_array_equal(_np(r["canvas"]), ls["canvas"])
+    np.testing.assert_array_equal(_np(r["step"]), ls["step"])
+    assert r["left"] == ls["left"]
+    if ls["diverged"]:
+        note("    a near-tie decision differed from the oracle: whole-loop comparison not applicable")
+        return
+    od = O.decode_loop(w.hidden, w.w_u, w.mask, w.cfg.dtype, P)
+    assert r["iterations"] == od["iterations"]
+    np.testing.assert_array_equal(_np(r["canvas"]), od["canvas"])
+    np.testing.assert_array_equal(_np(r["step"]), _oracle_steps(od, w.mask.shape))
+
+
+def test_decode_loop_max_iter_and_resume_state():
+    # a run cut at three iterations leaves exactly the first three iterations of the full run
+    w = make_workload(CONFIGS["tiny"].with_(sharp=("ushape", 12.0)), 3)
+    tensors = to_device(w)
+    full = rpd.Decoder(*tensors, gpu_params(O.LLADA)).run()
+    part = rpd.Decoder(*tensors, gpu_params(O.LLADA)).run(max_iter=3)
+    torch.cuda.synchronize()
+    assert part["iterations"] == 3 and part["left"] == full["left"][:3]
+    fs, ps = _np(full["step"]), _np(part["step"])
+    np.testing.assert_array_equal(ps, np.where(fs < 3, fs, -1))
+    np.testing.assert_array_equal(_np(part["canvas"]), np.where(fs < 3, _np(full["canvas"]), -1))
+    np.testing.assert_array_equal(_np(part["mask"]), ((w.mask != 0) & ((fs >= 3) | (fs < 0))).astype(np.uint8))
+
+
+def test_decode_loop_with_final_normalization():
+    cfg = CONFIGS["llada_late"].with_(name="decn", B=1, L=64, K=3, d=136, V=2003, n_masked=None, masked_frac=1.0,
+                                      sharp=("ushape", 12.0), unstable_frac=0.3)
+    w = make_workload(cfg, 8)
+    gain = round_bf16_bits(np.random.default_rng(9).uniform(0.5, 2.0, cfg.d))
+    norm = (gain, 1e-5, False)
+    tensors = to_device(w)
+    dec = rpd.Decoder(*tensors, gpu_params(O.LLADA), norm_weight=gain_tensor(w, gain), norm_eps=1e-5)
+    r = dec.run()
+    torch.cuda.synchronize()
+    ls = _lockstep(w, O.LLADA, dec.bounds[:r["iterations"]], tensors, norm=norm)
+    np.testing.assert_array_equal(_np(r["step"]), ls["step"])
+    np.testing.assert_array_equal(_np(r["canvas"]), ls["canvas"])
+    if not ls["diverged"]:
+        od = O.decode_loop(w.hidden, w.w_u, w.mask, w.cfg.dtype, O.LLADA,
+                           norm=(gain, float(np.float32(1e-5)), False))
+        np.testing.assert_array_equal(_np(r["step"]), _oracle_steps(od, w.mask.shape))
+
+
+def test_decode_loop_lazy_projection():
+    # lazy layerwise projection (eager only: it reads counts back inside the call) commits as the
+    # eager projection does
+    w = make_workload(CONFIGS["llada_late"].with_(name="decl", B=1, L=80, K=4, d=200, V=2503, n_masked=None,
+                                                  masked_frac=1.0, sharp=("calibrated",), unstable_frac=0.3), 10)
+    P = O.Params(theta_s=2.5, w=5.0, beta=2.0)
+    tensors = to_device(w)
+    eager = rpd.Decoder(*tensors, gpu_params(P)).run()
+    dl = rpd.Decoder(*tensors, gpu_params(dataclasses.replace(P, lazy=True)), graph=True)
+    assert not dl.graph
+    lazy = dl.run()
+    torch.cuda.synchronize()
+    note(f"    lazy iterations {lazy['iterations']} eager {eager['iterations']}")
+    od = O.decode_loop(w.hidden, w.w_u, w.mask, w.cfg.dtype, dataclasses.replace(P, lazy=True))
+    ost = _oracle_steps(od, w.mask.shape)
+    # both GPU projections agree with the oracle's lazy loop unless a near-tie decided otherwise, which the
+    # per-call lazy parity tests cover; here the seed has none
+    np.testing.assert_array_equal(_np(lazy["step"]), ost)
+    np.testing.assert_array_equal(_np(eager["step"]), ost)
+    np.testing.assert_array_equal(_np(lazy["canvas"]), od["canvas"])
