@@ -224,8 +224,7 @@ rpd_status rpd_score_commit(const rpd_problem* p, const rpd_params* q, const rpd
  * projection (logit lens + fused softmax statistics; with a norm_weight, the
  * final normalization of the rows comes first, after [1]), [2] after it, [3]
  * after the cross-tile reduction and stability scoring, [4] after the
- * commitment scan (with B == 1 the commitment runs inside the reduction
- * kernel, so [3] and [4] coincide). Only the first n_events (0..5) are used;
+ * commitment scan. Only the first n_events (0..5) are used;
  * NULL entries are skipped (with RPD_PARAM_LAZY, [1] precedes the first
  * pass and [2] follows the last). Everything else is exactly
  * rpd_score_commit.
@@ -256,9 +255,8 @@ enum {
   RPD_PROJ_BF16_S64 = 1,  /* bf16, 33..64 rows, same kernel family */
   RPD_PROJ_BF16_S128 = 2, /* bf16, 65..128 rows */
   RPD_PROJ_F32 = 3,       /* fp32 inputs, any row count */
-  RPD_PROJ_BF16_BIG = 4,  /* bf16, more than 256 rows: MFMA-bound 256 x 256 tiles */
-  RPD_PROJ_BF16_S192 = 5, /* bf16, 129..192 rows */
-  RPD_PROJ_BF16_S256 = 6  /* bf16, 193..256 rows */
+  RPD_PROJ_BF16_BIG = 4,  /* bf16, more than 192 rows: MFMA-bound 256 x 256 tiles */
+  RPD_PROJ_BF16_S192 = 5  /* bf16, 129..192 rows */
 };
 
 /*

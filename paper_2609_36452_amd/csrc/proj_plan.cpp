@@ -18,16 +18,15 @@ ProjPlan plan_projection(int dtype, long long rows_cap, int V) {
     p.grid = p.nvt * p.nrt;
     return p;
   }
-  if (rows_cap <= 256) {
+  if (rows_cap <= kStreamMaxRows) {
     // HBM-bound: one row tile holding every projected row, so W_U is read
     // once; a multiple of 256 equal vocabulary tiles, so every CU streams the
     // same share
     p.variant = rows_cap <= 32    ? PROJ_BF16_S32
                 : rows_cap <= 64  ? PROJ_BF16_S64
                 : rows_cap <= 128 ? PROJ_BF16_S128
-                : rows_cap <= 192 ? PROJ_BF16_S192
-                                  : PROJ_BF16_S256;
-    p.rows_per_tile = rows_cap <= 32 ? 32 : rows_cap <= 64 ? 64 : rows_cap <= 128 ? 128 : rows_cap <= 192 ? 192 : 256;
+                                  : PROJ_BF16_S192;
+    p.rows_per_tile = rows_cap <= 32 ? 32 : rows_cap <= 64 ? 64 : rows_cap <= 128 ? 128 : 192;
     p.vocab_cap = kStreamTileVocab;
     int nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
     nvt = ((nvt + 255) / 256) * 256;
@@ -51,8 +50,7 @@ hipError_t launch_projection(const Launch& a, hipStream_t s) {
     case PROJ_BF16_S32:
     case PROJ_BF16_S64:
     case PROJ_BF16_S128:
-    case PROJ_BF16_S192:
-    case PROJ_BF16_S256: return launch_proj_stream(a, s);
+    case PROJ_BF16_S192: return launch_proj_stream(a, s);
     case PROJ_BF16_BIG: return launch_proj_big(a, s);
     case PROJ_F32: return launch_proj_f32(a, s);
   }

@@ -18,7 +18,6 @@ struct CompactArgs {
   int32_t* n;
   int32_t* dev_status;
   int32_t* user_status;
-  int32_t* done;
 };
 
 template <int NW>
@@ -52,7 +51,6 @@ __device__ int compact_in_workgroup(const CompactArgs& ca, int* s_pos, int need,
     *ca.n = n;
     *ca.dev_status = st;
     if (ca.user_status) *ca.user_status = st;
-    *ca.done = 0;   // completion counter of the fused reduction + commitment
   }
   return n;
 }
@@ -81,9 +79,10 @@ __device__ int compact_in_workgroup(const CompactArgs& ca, int* s_pos, int need,
 // vocabulary row 32*mv + 8*(q >> 2) + 4*(l >> 5) + (q & 3) of the wave's
 // block and projected row 32*nb + (l & 31).
 //
-// Measured at the LLaDA-8B shape (d = 4096, V = 126464): 156 us at 32 rows
-// (83% of 8 TB/s), 159 us at 64, 180 us at 128, 211 us at 192, 246 us at
-// 256; the 256 x 256 MFMA tile needs 298 us at 256 rows.
+// Measured at the LLaDA-8B shape (d = 4096, V = 126464; projection alone,
+// best of several runs on one GPU): 156 us at 32 rows (83% of 8 TB/s),
+// 164 us at 64, 187-195 us at 104-128, 266-268 us at 160-192. Above 192 rows
+// the 256 x 256 MFMA tile is faster.
 //
 // FC: the workgroup compacts the mask itself (compact_in_workgroup).
 template <int NW, int MV, int NB, bool FC>
@@ -293,7 +292,7 @@ template <int NW, int MV, int NB>
 void launch_stream(const Launch& a, hipStream_t s) {
   static_assert(32 * MV * NW == kStreamTileVocab, "every streaming variant covers the same vocabulary tile");
   const ProjPlan& p = a.plan;
-  const CompactArgs ca{a.mask, a.B * a.L, a.max_masked, a.rows, a.n_masked, a.dev_status, a.user_status, a.done};
+  const CompactArgs ca{a.mask, a.B * a.L, a.max_masked, a.rows, a.n_masked, a.dev_status, a.user_status};
   if (a.fused_compact)
     hipLaunchKernelGGL((k_proj_bf16_stream<NW, MV, NB, true>), dim3(p.grid), dim3(NW * 64), 0, s,
                        static_cast<const uint16_t*>(a.hidden), static_cast<const uint16_t*>(a.w_u), a.rows,
@@ -310,8 +309,7 @@ void launch_stream(const Launch& a, hipStream_t s) {
 
 bool compact_fused(const Launch& a) {
   const ProjVariant v = a.plan.variant;
-  const bool streaming = v == PROJ_BF16_S32 || v == PROJ_BF16_S64 || v == PROJ_BF16_S128 || v == PROJ_BF16_S192 ||
-                         v == PROJ_BF16_S256;
+  const bool streaming = v == PROJ_BF16_S32 || v == PROJ_BF16_S64 || v == PROJ_BF16_S128 || v == PROJ_BF16_S192;
   return streaming && a.plan.nrt == 1 && a.max_masked > 0 && (long long)a.B * a.L <= kFusedCompactMax &&
          !a.xrows && !a.rowoff;   // the normalization and explicit row lists need the compaction first
 }
@@ -322,7 +320,6 @@ hipError_t launch_proj_stream(const Launch& a, hipStream_t s) {
     case PROJ_BF16_S64: launch_stream<4, 2, 2>(a, s); break;
     case PROJ_BF16_S128: launch_stream<8, 1, 4>(a, s); break;
     case PROJ_BF16_S192: launch_stream<8, 1, 6>(a, s); break;
-    case PROJ_BF16_S256: launch_stream<8, 1, 8>(a, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -21,7 +21,7 @@ rpd_status fail(rpd_status s, const char* fmt, ...) {
   return s;
 }
 
-constexpr size_t kHeaderBytes = 256;   // n_masked, device status, completion counter, lazy pass rows
+constexpr size_t kHeaderBytes = 256;   // n_masked (0), device status (4), lazy pass rows (12)
 constexpr long long kMaxBL = 1LL << 24;
 constexpr int kMaxK = 64;
 
@@ -230,7 +230,6 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
   a.max_masked = (int)cap;
   a.n_masked = reinterpret_cast<int32_t*>(ws);
   a.dev_status = reinterpret_cast<int32_t*>(ws + 4);
-  a.done = reinterpret_cast<int32_t*>(ws + 8);
   a.rows = reinterpret_cast<int32_t*>(ws + kHeaderBytes);
   a.partials = reinterpret_cast<float4*>(ws + kHeaderBytes + align256((size_t)((long long)p->B * p->L) * 4));
   a.norm_weight = p->norm_weight;
@@ -287,7 +286,7 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
   } else if ((e = mark(1)) == hipSuccess && (!a.xrows || (e = rpd::launch_norm_rows(a, s)) == hipSuccess) &&
              (e = rpd::launch_projection(a, s)) == hipSuccess && (e = mark(2)) == hipSuccess &&
              (e = rpd::launch_reduce_score(a, s)) == hipSuccess && (e = mark(3)) == hipSuccess &&
-             (rpd::commit_fused(a) || (e = rpd::launch_commit(a, s)) == hipSuccess)) {
+             (e = rpd::launch_commit(a, s)) == hipSuccess) {
     e = mark(4);
   }
   if (e != hipSuccess) return fail(RPD_ERR_HIP, "launch: %s", hipGetErrorString(e));

@@ -16,15 +16,17 @@ enum ProjVariant {
   PROJ_BF16_S64 = 1,    // <= 64 rows, same kernel family
   PROJ_BF16_S128 = 2,   // <= 128 rows
   PROJ_F32 = 3,         // fp32 inputs: vector ALU, 16 rows x 64 vocab
-  PROJ_BF16_BIG = 4,    // > 256 rows, MFMA-bound: 256 x 256 tiles, both operands staged through LDS
+  PROJ_BF16_BIG = 4,    // > 192 rows, MFMA-bound: 256 x 256 tiles, both operands staged through LDS
   PROJ_BF16_S192 = 5,   // <= 192 rows
-  PROJ_BF16_S256 = 6,   // <= 256 rows
 };
 
 // tile of the large-row variant: vocabulary rows x projected rows
 constexpr int kBigTileVocab = 256, kBigTileRows = 256;
 // vocabulary rows of one workgroup of the streaming variants (all of them)
 constexpr int kStreamTileVocab = 256;
+// most projected rows a streaming variant takes; above, the 256 x 256 tile
+// is faster (measured at 224 and 256 rows at the LLaDA-8B shape)
+constexpr int kStreamMaxRows = 192;
 // largest canvas (B * L) whose compaction the streaming projection does itself
 constexpr int kFusedCompactMax = 2048;
 
@@ -81,7 +83,6 @@ struct Launch {
   // workspace pieces
   int32_t* n_masked;     // [1] device count (clamped to max_masked)
   int32_t* dev_status;   // [1] internal status word
-  int32_t* done;         // [1] completion counter of the fused reduction + commitment
   bool fused_compact;    // the projection kernel does the compaction (no launch_compact)
   int32_t* rows;         // [max_masked] compacted b*L+i
   float4* partials;      // [K*max_masked][nvt]
@@ -112,14 +113,11 @@ struct Launch {
 };
 
 // enqueue, in this order: compaction, projection, reduction + scoring,
-// commitment (the last three use a.plan and a.max_masked). When
-// commit_fused(a), the reduction kernel's last workgroup runs the commitment
-// and launch_commit is not called.
+// commitment (the last three use a.plan and a.max_masked)
 hipError_t launch_compact(const Launch& a, hipStream_t s);
 hipError_t launch_projection(const Launch& a, hipStream_t s);
 hipError_t launch_reduce_score(const Launch& a, hipStream_t s);
 hipError_t launch_commit(const Launch& a, hipStream_t s);
-bool commit_fused(const Launch& a);
 
 // lazy layerwise projection: list the rows of layer l (first: every position),
 // reduce a pass over layer l, score from the per-position state
@@ -133,7 +131,7 @@ bool compact_fused(const Launch& a);
 // the projection variants, dispatched by launch_projection on a.plan.variant
 // the final normalization of the compacted rows into a.xrows (before the projection)
 hipError_t launch_norm_rows(const Launch& a, hipStream_t s);
-hipError_t launch_proj_stream(const Launch& a, hipStream_t s);  // PROJ_BF16_S32 .. PROJ_BF16_S256
+hipError_t launch_proj_stream(const Launch& a, hipStream_t s);  // PROJ_BF16_S32 .. PROJ_BF16_S192
 hipError_t launch_proj_big(const Launch& a, hipStream_t s);     // PROJ_BF16_BIG
 hipError_t launch_proj_f32(const Launch& a, hipStream_t s);     // PROJ_F32
 

@@ -13,7 +13,7 @@ namespace {
 __global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ mask, int BL, int cap,
                                                    int32_t* __restrict__ rows, int32_t* __restrict__ n_out,
                                                    int32_t* __restrict__ dev_status,
-                                                   int32_t* __restrict__ user_status, int32_t* __restrict__ done) {
+                                                   int32_t* __restrict__ user_status) {
   __shared__ int wsum[16];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
   int carry = 0;
@@ -43,7 +43,6 @@ __global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ ma
     }
     *n_out = n;
     *dev_status = st;
-    *done = 0;   // completion counter of the fused reduction + commitment
     if (user_status) *user_status = st;
   }
 }
@@ -385,24 +384,22 @@ __global__ __launch_bounds__(kCommitThreads) void k_commit(const uint8_t* __rest
 
 // K2: one workgroup of four waves per masked position. Wave w merges the
 // vocab-tile states of layers w, w+4, ... (wave_merge_row); wave 0 then
-// evaluates persistence, drop and stability with one lane per layer. With
-// FUSE (a batch of one sequence), the last workgroup to finish, found with a
-// device-scope counter that the compaction zeroed, also runs the commitment
-// (K3), which saves its launch.
-template <bool FUSE>
+// evaluates persistence, drop and stability with one lane per layer. The
+// commitment (K3) follows as its own launch: handing it to the last
+// workgroup to finish instead needs a device-scope release and acquire in
+// every workgroup (an L2 write-back and invalidate each), which measured
+// slower than the launch.
 __global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4* __restrict__ partials,
                                                                      const int32_t* __restrict__ rows,
                                                                      const int32_t* __restrict__ n_ptr, int nvt,
-                                                                     ScoreArgs a, const uint8_t* __restrict__ mask,
-                                                                     CommitArgs ca, int32_t* __restrict__ done) {
+                                                                     ScoreArgs a) {
   __shared__ int ly[64];
   __shared__ float lc[64], lh[64];
-  __shared__ int s_last;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int p = blockIdx.x;
   const int n = *n_ptr;
-  if (!FUSE && p >= n) return;
-  if (p < n) {
+  if (p >= n) return;
+  {
     const int pos = rows[p];
     const int b = pos / a.L, i = pos - b * a.L;
     for (int l = wid; l < a.K; l += kReduceWaves) {
@@ -447,14 +444,6 @@ __global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4
       }
     }
   }
-  if (!FUSE) return;
-  __threadfence();   // this workgroup's outputs, visible device-wide before it is counted
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = p < n ? (atomicAdd(done, 1) == n - 1) : (n == 0 && p == 0);
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();   // every other workgroup's outputs are visible from here on
-  commit_sequence(mask, ca, 0, GlobalScores{ca.flags, ca.entropy, ca.confidence});
 }
 
 // End of an iteration (Section 3.2): committed positions take their token in
@@ -544,20 +533,14 @@ CommitArgs commit_args(const Launch& a) {
 
 hipError_t launch_compact(const Launch& a, hipStream_t s) {
   hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, a.mask, a.B * a.L, a.max_masked, a.rows, a.n_masked,
-                     a.dev_status, a.user_status, a.done);
+                     a.dev_status, a.user_status);
   return hipGetLastError();
 }
 
-bool commit_fused(const Launch& a) { return a.B == 1 && a.max_masked > 0; }
-
 hipError_t launch_reduce_score(const Launch& a, hipStream_t s) {
   if (a.max_masked <= 0) return hipSuccess;
-  if (commit_fused(a))
-    hipLaunchKernelGGL(k_reduce_score<true>, dim3(a.max_masked), dim3(64 * kReduceWaves), 0, s, a.partials, a.rows,
-                       a.n_masked, a.plan.nvt, score_args(a), a.mask, commit_args(a), a.done);
-  else
-    hipLaunchKernelGGL(k_reduce_score<false>, dim3(a.max_masked), dim3(64 * kReduceWaves), 0, s, a.partials,
-                       a.rows, a.n_masked, a.plan.nvt, score_args(a), a.mask, commit_args(a), a.done);
+  hipLaunchKernelGGL(k_reduce_score, dim3(a.max_masked), dim3(64 * kReduceWaves), 0, s, a.partials, a.rows,
+                     a.n_masked, a.plan.nvt, score_args(a));
   return hipGetLastError();
 }
 

@@ -76,7 +76,7 @@ def test_projection_variant_thresholds():
     pv = lambda n, dt=rpd.DTYPE_BF16: rpd.projection_variant(4, 1, 256, 4096, 126464, dt, max_masked=n)  # noqa: E731
     assert [pv(n) for n in (1, 8, 9, 16, 17, 32, 33, 48, 49, 64, 65, 256)] == \
         ["bf16_s32", "bf16_s32", "bf16_s64", "bf16_s64", "bf16_s128", "bf16_s128", "bf16_s192", "bf16_s192",
-         "bf16_s256", "bf16_s256", "bf16_big", "bf16_big"]
+         "bf16_big", "bf16_big", "bf16_big", "bf16_big"]
     assert pv(8, rpd.DTYPE_F32) == "f32" and pv(256, rpd.DTYPE_F32) == "f32"
     assert pv(-1) == "bf16_big"          # -1 plans for every position masked
     with pytest.raises(rpd.RpdError):

@@ -66,7 +66,7 @@ BF16_CASES = [
     ("bf16_s64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10, masked_frac=None), 12),
     ("bf16_s128_long_d", dict(B=1, L=40, K=4, d=4104, V=2500, n_masked=20, masked_frac=None), 15),
     ("bf16_s192_two_seqs", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=20, masked_frac=None), 16),
-    ("bf16_s256_odd_chunks", dict(B=1, L=80, K=3, d=200, V=6007, n_masked=80, masked_frac=None), 17),
+    ("bf16_big_one_row_tile_odd_chunks", dict(B=1, L=80, K=3, d=200, V=6007, n_masked=80, masked_frac=None), 17),
     ("bf16_big_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
     ("bf16_big_row_split", dict(B=4, L=600, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
 ]
@@ -115,7 +115,7 @@ def _gain(w, seed):
     return round_bf16_bits(g) if w.cfg.dtype == "bf16" else g.astype(np.float32)
 
 
-NORM_CASES = [c for c in BF16_CASES if c[0] in ("bf16_s32", "bf16_s128_long_d", "bf16_s256_odd_chunks",
+NORM_CASES = [c for c in BF16_CASES if c[0] in ("bf16_s32", "bf16_s128_long_d", "bf16_big_one_row_tile_odd_chunks",
                                                "bf16_big_vocab_split")]
 
 
