@@ -75,13 +75,15 @@ def read_traffic(variant: str, workload: str):
 
 def copy_probe(torch) -> float:
     """A plain streaming copy of known size (read COPY_PROBE_BYTES, write as
-    many) for scaling the HBM byte counters: three launches of torch.neg on
-    fp32 buffers far larger than the last-level cache. Returns the copy's
+    many) for scaling the HBM byte counters: three timed launches of torch.neg
+    on fp32 buffers far larger than the last-level cache (after one that
+    loads the kernel). Returns the copy's
     HBM rate in GB/s (bytes read + written over the average launch), a
     reference for what this particular GPU streams."""
     n = COPY_PROBE_BYTES // 4
     src = torch.ones(n, dtype=torch.float32, device="cuda:0")
     dst = torch.empty_like(src)
+    torch.neg(src, out=dst)        # the first launch loads the kernel
     torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record()
