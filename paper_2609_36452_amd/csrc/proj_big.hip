@@ -12,9 +12,12 @@ namespace {
 //
 // Operands move global -> registers -> LDS -> MFMA fragments. A 32-wide
 // k-chunk of both operands (256 rows x 64 bytes each) is loaded into
-// registers two chunks ahead (16 B per lane, a wave instruction covering 16
+// registers three chunks ahead (16 B per lane, a wave instruction covering 16
 // rows x 64 bytes), written to one of two LDS stages, and read back as MFMA
-// fragments. Within a tile row the four 16-byte pieces are stored XOR-
+// fragments. With one wave per SIMD nothing else hides the load latency:
+// three chunks in flight instead of two measured 4-5% faster from 512 rows up
+// (the register slots rotate with period 3 against the stages' period 2, so
+// the loop is unrolled six times to keep every slot index static). Within a tile row the four 16-byte pieces are stored XOR-
 // swizzled by (row >> 2) & 3 (chosen through which global piece each lane
 // fetches), so the fragment reads are free of bank conflicts.
 //
@@ -28,13 +31,13 @@ namespace {
 // groups so that one memory instruction issues between consecutive MFMAs:
 //   first half:  MFMAs of k-step (c,0), interleaved with the fragment reads
 //                of (c,1), the LDS writes of chunk c+1 and the global loads
-//                of chunk c+3;
+//                of chunk c+4;
 //   barrier:     publishes chunk c+1 and frees stage c & 1;
 //   second half: MFMAs of (c,1), interleaved with the fragment reads of
 //                (c+1,0).
 namespace big {
 constexpr int TV = kBigTileVocab, TR = kBigTileRows, KC = 32;
-constexpr int D = 2;   // chunks in flight in registers
+constexpr int D = 3;   // chunks in flight in registers
 }  // namespace big
 
 __global__ __launch_bounds__(256) void k_proj_bf16_big(
@@ -43,7 +46,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     int nvt, int nrt, int split_rows, const uint16_t* __restrict__ xrows, const long long* __restrict__ rowoff,
     float scale) {
   using namespace big;
-  static_assert(TV == 256 && TR == 256 && D == 2, "wave layout and register ring below assume these");
+  static_assert(TV == 256 && TR == 256 && D == 3, "wave layout and register ring below assume these");
   __shared__ __attribute__((aligned(16))) uint16_t sa0[TV][KC], sa1[TV][KC];
   __shared__ __attribute__((aligned(16))) uint16_t sb0[TR][KC], sb1[TR][KC];
   __shared__ float4 red[2][TR];
@@ -166,12 +169,21 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     RPD_LOAD(0, min(D, nchf - 1));
     __syncthreads();
     RPD_FRAGS(fa0, fb0, 0, 0);
+    // chunk c: stage c & 1, register slot (c + 1) % 3
     int c = 0;
-    for (; c + 2 <= nchf; c += 2) {
+    for (; c + 6 <= nchf; c += 6) {
       RPD_CHUNK(c, 0, 1);
-      RPD_CHUNK(c + 1, 1, 0);
+      RPD_CHUNK(c + 1, 1, 2);
+      RPD_CHUNK(c + 2, 0, 0);
+      RPD_CHUNK(c + 3, 1, 1);
+      RPD_CHUNK(c + 4, 0, 2);
+      RPD_CHUNK(c + 5, 1, 0);
     }
     if (c < nchf) RPD_CHUNK(c, 0, 1);
+    if (c + 1 < nchf) RPD_CHUNK(c + 1, 1, 2);
+    if (c + 2 < nchf) RPD_CHUNK(c + 2, 0, 0);
+    if (c + 3 < nchf) RPD_CHUNK(c + 3, 1, 1);
+    if (c + 4 < nchf) RPD_CHUNK(c + 4, 0, 2);
   }
   if (d % KC != 0) {   // partial last chunk, zero-filled past d (d % 8 == 0: a piece is all in or all out)
     __syncthreads();   // every wave is done with both stages
