@@ -1,4 +1,4 @@
-// K1 projection, bf16, large row counts (more than 256 projected rows): the
+// K1 projection, bf16, large row counts (more than 192 projected rows): the
 // MFMA-bound regime.
 #include "rpd_device.h"
 
@@ -10,35 +10,36 @@ namespace {
 // with v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane in AGPRs,
 // one wave per SIMD).
 //
-// Operands move global -> registers -> LDS -> MFMA fragments. A 32-wide
-// k-chunk of both operands (256 rows x 64 bytes each) is loaded into
-// registers three chunks ahead (16 B per lane, a wave instruction covering 16
-// rows x 64 bytes), written to one of two LDS stages, and read back as MFMA
-// fragments. With one wave per SIMD nothing else hides the load latency:
-// three chunks in flight instead of two measured 4-5% faster from 512 rows up
-// (the register slots rotate with period 3 against the stages' period 2, so
-// the loop is unrolled six times to keep every slot index static). Within a tile row the four 16-byte pieces are stored XOR-
-// swizzled by (row >> 2) & 3 (chosen through which global piece each lane
-// fetches), so the fragment reads are free of bank conflicts.
+// Operands go from global memory straight into LDS (global_load_lds_dwordx4:
+// each instruction deposits 64 lanes x 16 B = 8 rows x 128 B of one operand
+// at the LDS address in M0), in 64-wide k-chunks over two LDS stages of
+// 2 x 256 rows x 128 B, and are read back as MFMA fragments. No register
+// staging and no LDS store instructions: with them, the LDS instruction
+// queue saturated (counters showed its data FIFO full for 1.2e7 cycles per
+// call at 1024 rows), and staging 96 registers of loads left no room for a
+// deeper pipeline. The eight 16-byte pieces of row r sit XOR-swizzled by
+// (r >> 1) & 7 (each lane fetches the global piece that belongs at its LDS
+// slot), which keeps the fragment reads free of bank conflicts.
 //
-// Plain loads into registers rather than direct global->LDS loads: with one
-// wave per SIMD, direct loads sustain about 17 B/clk per CU, below the
-// 32 B/clk this tile needs at full MFMA rate, and being opaque to the
-// compiler's scheduler they cannot be spread between MFMAs; register loads
-// sustain about 26 B/clk and interleave.
+// Chunk c lives in stage c & 1 and is multiplied in four k-steps of 16
+// MFMAs; each step reads the fragments of the next while multiplying. After
+// the third step every wave waits for its own loads of chunk c+1 and for its
+// fragment reads, and one barrier then publishes chunk c+1 and frees stage
+// c & 1; the fourth step reads the first fragments of chunk c+1 and issues
+// the loads of chunk c+2 into the freed stage, so a load has three k-steps
+// (48 MFMAs) to land. The barrier is a plain s_barrier: the waits before it
+// are exactly the ones this schedule needs, where a fenced barrier would
+// also drain the loads still in flight. One barrier per 64 MFMAs.
 //
-// Per chunk c (stage c & 1), the instruction stream is fixed with scheduling
-// groups so that one memory instruction issues between consecutive MFMAs:
-//   first half:  MFMAs of k-step (c,0), interleaved with the fragment reads
-//                of (c,1), the LDS writes of chunk c+1 and the global loads
-//                of chunk c+4;
-//   barrier:     publishes chunk c+1 and frees stage c & 1;
-//   second half: MFMAs of (c,1), interleaved with the fragment reads of
-//                (c+1,0).
+// Measured against the previous form (loads staged through registers in
+// 32-wide chunks, three in flight): 6% faster at 1024 rows, 4-5% at 4096 and
+// 12288, no change at 256.
 namespace big {
-constexpr int TV = kBigTileVocab, TR = kBigTileRows, KC = 32;
-constexpr int D = 3;   // chunks in flight in registers
+constexpr int TV = kBigTileVocab, TR = kBigTileRows, KC = 64;
 }  // namespace big
+
+// s_waitcnt immediate: vmcnt <= n, lgkmcnt == 0, expcnt unconstrained
+constexpr unsigned vm_lgkm_wait(int n) { return (unsigned)((n & 15) | ((n >> 4) << 14) | (7 << 4)); }
 
 __global__ __launch_bounds__(256) void k_proj_bf16_big(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
@@ -46,12 +47,12 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     int nvt, int nrt, int split_rows, const uint16_t* __restrict__ xrows, const long long* __restrict__ rowoff,
     float scale) {
   using namespace big;
-  static_assert(TV == 256 && TR == 256 && D == 3, "wave layout and register ring below assume these");
-  __shared__ __attribute__((aligned(16))) uint16_t sa0[TV][KC], sa1[TV][KC];
-  __shared__ __attribute__((aligned(16))) uint16_t sb0[TR][KC], sb1[TR][KC];
+  static_assert(TV == 256 && TR == 256, "wave layout below assumes a 256 x 256 tile");
+  __shared__ __attribute__((aligned(1024))) uint16_t sa0[TV][KC], sa1[TV][KC];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb0[TR][KC], sb1[TR][KC];
   __shared__ float4 red[2][TR];
-#define RPD_SA(S) ((S) == 0 ? sa0 : sa1)
-#define RPD_SB(S) ((S) == 0 ? sb0 : sb1)
+#define RPD_SA(X) ((X) == 0 ? sa0 : sa1)
+#define RPD_SB(X) ((X) == 0 ? sb0 : sb1)
 
   int rt, vt;
   if (!map_job(blockIdx.x, nvt, nrt, split_rows, rt, vt)) return;
@@ -63,32 +64,35 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wv = wid & 1, wr = wid >> 1;
 
-  // load sources: instruction u of this wave covers tile rows
-  // 64*wid + 16*u .. +16; lane l holds LDS piece (l & 3) of row (l >> 2),
-  // fetched from the global piece (l & 3) ^ swizzle(row)
-  long long ga[4], gb[4];
+  // load sources: instruction u of this wave covers tile rows 64*wid + 8*u ..
+  // +8; lane l lands at LDS piece (l & 7) of row (l >> 3) and fetches the
+  // global piece (l & 7) ^ swizzle(row). Rows past the tile re-read its last
+  // vocabulary row, rows past the last projected row re-read row r0 (both
+  // discarded at the end).
+  const uint16_t* pa[8];
+  const uint16_t* pb[8];
+  const uint16_t* __restrict__ xsrc = xrows ? xrows : hidden;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int tr = 64 * wid + 16 * u + (lane >> 2);
-    const int piece = (lane & 3) ^ ((tr >> 2) & 3);
-    ga[u] = (long long)min(vb + tr, ve - 1) * d + piece * 8;
-    const int r = r0 + tr < R ? r0 + tr : r0;   // padding rows re-read a real row; discarded at the end
+  for (int u = 0; u < 8; ++u) {
+    const int tr = 64 * wid + 8 * u + (lane >> 3);
+    const int piece = (lane & 7) ^ ((tr >> 1) & 7);
+    pa[u] = w_u + (long long)min(vb + tr, ve - 1) * d + piece * 8;
+    const int r = r0 + tr < R ? r0 + tr : r0;
+    long long ob;
     if (xrows) {   // normalized rows, already in projected-row order
-      gb[u] = (long long)r * d + piece * 8;
+      ob = (long long)r * d + piece * 8;
     } else if (rowoff) {   // an explicit row list
-      gb[u] = rowoff[r] + piece * 8;
+      ob = rowoff[r] + piece * 8;
     } else {
       const int p = r / K, l = r - p * K;
       const int pos = rows[p];
       const int b = pos / L, i = pos - b * L;
-      gb[u] = (((long long)l * B + b) * L + i) * (long long)d + piece * 8;
+      ob = (((long long)l * B + b) * L + i) * (long long)d + piece * 8;
     }
+    pb[u] = xsrc + ob;
   }
-  const uint16_t* __restrict__ xsrc = xrows ? xrows : hidden;
-  const int srow = lane >> 2, scol = (lane & 3) * 8;
   // fragment reads: lane reads row base + (lane & 31), logical piece 2s + (lane >> 5)
-  const int swl = ((lane & 31) >> 2) & 3;
-  const int fcol0 = 8 * ((0 + (lane >> 5)) ^ swl), fcol1 = 8 * ((2 + (lane >> 5)) ^ swl);
+  const int fr = lane & 31, fsw = (fr >> 1) & 7, fhi = lane >> 5;
 
   f32x16 acc[4][4];
 #pragma unroll
@@ -97,30 +101,24 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[mv][nb][q] = 0.f;
-  u32x4 ld[D][8];
   u32x4 fa0[4], fb0[4], fa1[4], fb1[4];
 
-#define RPD_LOAD(slot, chunk)                                                                             \
+#define RPD_DLOAD(X, chunk)                                                                               \
   do {                                                                                                    \
     const long long k0_ = (long long)(chunk) * KC;                                                        \
-    _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                                   \
-      ld[slot][u_] = *reinterpret_cast<const u32x4*>(w_u + ga[u_] + k0_);                                 \
-      ld[slot][4 + u_] = *reinterpret_cast<const u32x4*>(xsrc + gb[u_] + k0_);                            \
+    _Pragma("unroll") for (int u_ = 0; u_ < 8; ++u_) {                                                   \
+      __builtin_amdgcn_global_load_lds((const void*)(pa[u_] + k0_),                                       \
+          (__attribute__((address_space(3))) void*)&RPD_SA(X)[64 * wid + 8 * u_][0], 16, 0, 0);          \
+      __builtin_amdgcn_global_load_lds((const void*)(pb[u_] + k0_),                                       \
+          (__attribute__((address_space(3))) void*)&RPD_SB(X)[64 * wid + 8 * u_][0], 16, 0, 0);          \
     }                                                                                                     \
   } while (0)
-#define RPD_STORE(slot, stage)                                                                            \
+#define RPD_FRAGS(FA, FB, X, kstep)                                                                       \
   do {                                                                                                    \
-    _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                                   \
-      *reinterpret_cast<u32x4*>(&RPD_SA(stage)[64 * wid + 16 * u_ + srow][scol]) = ld[slot][u_];         \
-      *reinterpret_cast<u32x4*>(&RPD_SB(stage)[64 * wid + 16 * u_ + srow][scol]) = ld[slot][4 + u_];     \
-    }                                                                                                     \
-  } while (0)
-#define RPD_FRAGS(FA, FB, stage, kstep)                                                                   \
-  do {                                                                                                    \
-    const int fc_ = (kstep) ? fcol1 : fcol0;                                                              \
+    const int fc_ = 8 * ((2 * (kstep) + fhi) ^ fsw);                                                      \
     _Pragma("unroll") for (int m_ = 0; m_ < 4; ++m_) {                                                   \
-      FA[m_] = *reinterpret_cast<const u32x4*>(&RPD_SA(stage)[128 * wv + 32 * m_ + (lane & 31)][fc_]);   \
-      FB[m_] = *reinterpret_cast<const u32x4*>(&RPD_SB(stage)[128 * wr + 32 * m_ + (lane & 31)][fc_]);   \
+      FA[m_] = *reinterpret_cast<const u32x4*>(&RPD_SA(X)[128 * wv + 32 * m_ + fr][fc_]);                \
+      FB[m_] = *reinterpret_cast<const u32x4*>(&RPD_SB(X)[128 * wr + 32 * m_ + fr][fc_]);                \
     }                                                                                                     \
   } while (0)
 #define RPD_MMA(FA, FB)                                                                                   \
@@ -131,84 +129,86 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
                                                                __builtin_bit_cast(bf16x8, FB[nb_]),        \
                                                                acc[mv_][nb_], 0, 0, 0);                   \
   } while (0)
-  // one chunk c, held in stage ST; its successor goes to stage ST^1 from
-  // register slot SL, which is then refilled with chunk c+1+D. Chunks past
-  // the end repeat the last one (loaded and staged, never multiplied).
-#define RPD_CHUNK(c, ST, SL)                                                                              \
+  // 16 MFMAs with the 8 fragment reads of the next k-step between the first eight
+#define RPD_MIX()                                                                                         \
   do {                                                                                                    \
-    __builtin_amdgcn_sched_barrier(0);                                                                    \
-    RPD_FRAGS(fa1, fb1, ST, 1);                                                                           \
-    RPD_STORE(SL, (ST) ^ 1);                                                                              \
-    RPD_LOAD(SL, min((c) + 1 + D, nchf - 1));                                                             \
-    RPD_MMA(fa0, fb0);                                                                                    \
     _Pragma("unroll") for (int g_ = 0; g_ < 8; ++g_) {                                                   \
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */                                       \
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* LDS read */                                   \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */                                       \
-      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0); /* LDS write */                                  \
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0); /* global load */                                \
-    }                                                                                                     \
-    __builtin_amdgcn_sched_barrier(0);                                                                    \
-    __syncthreads();                                                                                      \
-    __builtin_amdgcn_sched_barrier(0);                                                                    \
-    RPD_FRAGS(fa0, fb0, (ST) ^ 1, 0);                                                                     \
-    RPD_MMA(fa1, fb1);                                                                                    \
-    _Pragma("unroll") for (int g_ = 0; g_ < 8; ++g_) {                                                   \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                                  \
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                                  \
     }                                                                                                     \
     __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                                                    \
+  } while (0)
+  // chunk c in stage X (fragments of its first k-step already in fa0/fb0)
+#define RPD_CHUNK(c, X)                                                                                   \
+  do {                                                                                                    \
+    __builtin_amdgcn_sched_barrier(0);                                                                    \
+    RPD_FRAGS(fa1, fb1, X, 1);                                                                            \
+    RPD_MMA(fa0, fb0);                                                                                    \
+    RPD_MIX();                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                                    \
+    RPD_FRAGS(fa0, fb0, X, 2);                                                                            \
+    RPD_MMA(fa1, fb1);                                                                                    \
+    RPD_MIX();                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                                    \
+    RPD_FRAGS(fa1, fb1, X, 3);                                                                            \
+    RPD_MMA(fa0, fb0);                                                                                    \
+    RPD_MIX();                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                                    \
+    __builtin_amdgcn_s_waitcnt(vm_lgkm_wait(0)); /* own loads of chunk c+1 landed, own reads of X done */ \
+    __builtin_amdgcn_s_barrier();                                                                         \
+    __builtin_amdgcn_sched_barrier(0);                                                                    \
+    RPD_FRAGS(fa0, fb0, (X) ^ 1, 0);                                                                      \
+    RPD_DLOAD(X, min((c) + 2, nchf - 1));                                                                 \
+    RPD_MMA(fa1, fb1);                                                                                    \
+    _Pragma("unroll") for (int g_ = 0; g_ < 16; ++g_) {                                                  \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */                                       \
+      if (g_ < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* LDS read */                       \
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0); /* global->LDS load */                           \
+    }                                                                                                     \
     __builtin_amdgcn_sched_barrier(0);                                                                    \
   } while (0)
 
+  // Chunks past the end repeat the last one (loaded, never multiplied).
   const int nchf = d / KC;
   if (nchf > 0) {
-#pragma unroll
-    for (int j = 0; j < D; ++j) RPD_LOAD(j, min(j, nchf - 1));
-    RPD_STORE(0, 0);
-    RPD_LOAD(0, min(D, nchf - 1));
-    __syncthreads();
+    RPD_DLOAD(0, 0);
+    RPD_DLOAD(1, min(1, nchf - 1));
+    __builtin_amdgcn_s_waitcnt(vm_lgkm_wait(16));   // this wave's loads of chunk 0 landed (chunk 1 in flight)
+    __builtin_amdgcn_s_barrier();
     RPD_FRAGS(fa0, fb0, 0, 0);
-    // chunk c: stage c & 1, register slot (c + 1) % 3
     int c = 0;
-    for (; c + 6 <= nchf; c += 6) {
-      RPD_CHUNK(c, 0, 1);
-      RPD_CHUNK(c + 1, 1, 2);
-      RPD_CHUNK(c + 2, 0, 0);
-      RPD_CHUNK(c + 3, 1, 1);
-      RPD_CHUNK(c + 4, 0, 2);
-      RPD_CHUNK(c + 5, 1, 0);
+    for (; c + 2 <= nchf; c += 2) {
+      RPD_CHUNK(c, 0);
+      RPD_CHUNK(c + 1, 1);
     }
-    if (c < nchf) RPD_CHUNK(c, 0, 1);
-    if (c + 1 < nchf) RPD_CHUNK(c + 1, 1, 2);
-    if (c + 2 < nchf) RPD_CHUNK(c + 2, 0, 0);
-    if (c + 3 < nchf) RPD_CHUNK(c + 3, 1, 1);
-    if (c + 4 < nchf) RPD_CHUNK(c + 4, 0, 2);
+    if (c < nchf) RPD_CHUNK(c, 0);
+    __builtin_amdgcn_s_waitcnt(vm_lgkm_wait(0));    // no load outstanding past the loop
+    __syncthreads();
   }
   if (d % KC != 0) {   // partial last chunk, zero-filled past d (d % 8 == 0: a piece is all in or all out)
-    __syncthreads();   // every wave is done with both stages
     const long long k0 = (long long)nchf * KC;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int tr = 64 * wid + 16 * u + srow;
-      const int piece = (lane & 3) ^ ((tr >> 2) & 3);
+    for (int u = 0; u < 8; ++u) {
+      const int tr = 64 * wid + 8 * u + (lane >> 3);
+      const int piece = (lane & 7) ^ ((tr >> 1) & 7);
       const bool in = k0 + piece * 8 < d;
-      const u32x4 va = in ? *reinterpret_cast<const u32x4*>(w_u + ga[u] + k0) : u32x4{0u, 0u, 0u, 0u};
-      const u32x4 vh = in ? *reinterpret_cast<const u32x4*>(xsrc + gb[u] + k0) : u32x4{0u, 0u, 0u, 0u};
-      *reinterpret_cast<u32x4*>(&sa0[tr][scol]) = va;
-      *reinterpret_cast<u32x4*>(&sb0[tr][scol]) = vh;
+      const u32x4 va = in ? *reinterpret_cast<const u32x4*>(pa[u] + k0) : u32x4{0u, 0u, 0u, 0u};
+      const u32x4 vh = in ? *reinterpret_cast<const u32x4*>(pb[u] + k0) : u32x4{0u, 0u, 0u, 0u};
+      *reinterpret_cast<u32x4*>(&sa0[tr][(lane & 7) * 8]) = va;
+      *reinterpret_cast<u32x4*>(&sb0[tr][(lane & 7) * 8]) = vh;
     }
     __syncthreads();
-    RPD_FRAGS(fa0, fb0, 0, 0);
-    RPD_MMA(fa0, fb0);
-    RPD_FRAGS(fa1, fb1, 0, 1);
-    RPD_MMA(fa1, fb1);
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+      RPD_FRAGS(fa0, fb0, 0, s4);
+      RPD_MMA(fa0, fb0);
+    }
   }
 #undef RPD_CHUNK
+#undef RPD_MIX
 #undef RPD_MMA
 #undef RPD_FRAGS
-#undef RPD_STORE
-#undef RPD_LOAD
+#undef RPD_DLOAD
 #undef RPD_SA
 #undef RPD_SB
 
