@@ -60,10 +60,11 @@ __device__ __forceinline__ Soft soft_empty() {
 }
 
 // S == 0 only for a state that has seen no vocabulary entry (a state with
-// one or more entries has S >= 1, or NaN).
+// one or more entries has S >= 1, or NaN). Merging with an empty state
+// returns the other one unchanged; the general formula is evaluated anyway
+// and the empty cases are chosen by selects, so that lanes holding states
+// of different kinds never branch.
 __device__ __forceinline__ Soft soft_merge(const Soft a, const Soft b) {
-  if (b.S == 0.f) return a;
-  if (a.S == 0.f) return b;
   const float M = fmaxf(a.m, b.m);
   const float da = a.m - M, db = b.m - M;
   const float ea = __expf(da), eb = __expf(db);
@@ -72,6 +73,11 @@ __device__ __forceinline__ Soft soft_merge(const Soft a, const Soft b) {
   r.S = a.S * ea + b.S * eb;
   r.T = (a.T + da * a.S) * ea + (b.T + db * b.S) * eb;
   r.idx = (a.m > b.m) ? a.idx : ((b.m > a.m) ? b.idx : min(a.idx, b.idx));
+  const bool a_empty = a.S == 0.f, b_empty = b.S == 0.f;
+  r.m = b_empty ? a.m : (a_empty ? b.m : r.m);
+  r.idx = b_empty ? a.idx : (a_empty ? b.idx : r.idx);
+  r.S = b_empty ? a.S : (a_empty ? b.S : r.S);
+  r.T = b_empty ? a.T : (a_empty ? b.T : r.T);
   return r;
 }
 
@@ -98,26 +104,31 @@ __device__ __forceinline__ Soft soft_unpack(const float4 v) {
 }
 
 // Statistics of N logits held by one lane, vocabulary indices increasing;
-// entries with valid == false are skipped. NaN logits never win the max and
-// turn S and T into NaN.
+// entries with valid == false add nothing. NaN logits never win the max and
+// turn S and T into NaN. Written with selects instead of branches (an
+// invalid entry adds an exact 0 to S and T), since the validity differs
+// from lane to lane and the branches cost more than the arithmetic.
 template <int N>
 __device__ __forceinline__ Soft soft_from_values(const float (&z)[N], const int (&v)[N], const bool (&ok)[N]) {
-  Soft s = soft_empty();
+  float m = -INFINITY;
+  int idx = INT_MAX;
 #pragma unroll
-  for (int e = 0; e < N; ++e)
-    if (ok[e] && z[e] > s.m) {
-      s.m = z[e];
-      s.idx = v[e];
-    }
+  for (int e = 0; e < N; ++e) {
+    const bool take = ok[e] && z[e] > m;
+    m = take ? z[e] : m;
+    idx = take ? v[e] : idx;
+  }
   float S = 0.f, T = 0.f;
 #pragma unroll
-  for (int e = 0; e < N; ++e)
-    if (ok[e]) {
-      const float dz = z[e] - s.m;
-      const float ex = __expf(dz);
-      S += ex;
-      T = fmaf(ex, dz, T);
-    }
+  for (int e = 0; e < N; ++e) {
+    const float dz = ok[e] ? z[e] - m : 0.f;
+    const float ex = ok[e] ? __expf(dz) : 0.f;
+    S += ex;
+    T = fmaf(ex, dz, T);
+  }
+  Soft s;
+  s.m = m;
+  s.idx = idx;
   s.S = S;
   s.T = T;
   return s;
