@@ -12,28 +12,35 @@ namespace {
 //
 // Operands go from global memory straight into LDS (global_load_lds_dwordx4:
 // each instruction deposits 64 lanes x 16 B = 8 rows x 128 B of one operand
-// at the LDS address in M0), in 64-wide k-chunks over two LDS stages of
-// 2 x 256 rows x 128 B, and are read back as MFMA fragments. No register
-// staging and no LDS store instructions: with them, the LDS instruction
-// queue saturated (counters showed its data FIFO full for 1.2e7 cycles per
-// call at 1024 rows), and staging 96 registers of loads left no room for a
-// deeper pipeline. The eight 16-byte pieces of row r sit XOR-swizzled by
-// (r >> 1) & 7 (each lane fetches the global piece that belongs at its LDS
-// slot), which keeps the fragment reads free of bank conflicts.
+// at the LDS address in M0), in 64-wide k-chunks, and are read back as MFMA
+// fragments. No register staging and no LDS store instructions: with them,
+// the LDS instruction queue saturated (counters showed its data FIFO full
+// for 1.2e7 cycles per call at 1024 rows). The eight 16-byte pieces of row r
+// sit XOR-swizzled by (r >> 1) & 7 (each lane fetches the global piece that
+// belongs at its LDS slot), which keeps the fragment reads free of bank
+// conflicts.
 //
-// Chunk c lives in stage c & 1 and is multiplied in four k-steps of 16
-// MFMAs; each step reads the fragments of the next while multiplying. After
-// the third step every wave waits for its own loads of chunk c+1 and for its
-// fragment reads, and one barrier then publishes chunk c+1 and frees stage
-// c & 1; the fourth step reads the first fragments of chunk c+1 and issues
-// the loads of chunk c+2 into the freed stage, so a load has three k-steps
-// (48 MFMAs) to land. The barrier is a plain s_barrier: the waits before it
-// are exactly the ones this schedule needs, where a fenced barrier would
-// also drain the loads still in flight. One barrier per 64 MFMAs.
+// Stages: three for W_U (32 KB each) and two for the hidden rows, which is
+// all 160 KB of LDS (the epilogue's reduction array reuses W_U stage 0). A
+// W_U chunk is first fetched from HBM by whichever of the workgroups sharing
+// it gets there first, while hidden rows mostly come from L2 or the MALL, so
+// W_U loads are issued two chunks earlier than hidden-row loads.
 //
-// Measured against the previous form (loads staged through registers in
-// 32-wide chunks, three in flight): 6% faster at 1024 rows, 4-5% at 4096 and
-// 12288, no change at 256.
+// Chunk c (W_U stage c % 3, hidden stage c % 2) is multiplied in four
+// k-steps of 16 MFMAs, each reading the next step's fragments. After the
+// third step every wave waits until only its newest 8 loads (W_U of chunk
+// c+2) may be outstanding, so chunk c+1 has landed, and for its fragment
+// reads; one barrier then publishes chunk c+1 and frees chunk c's stages.
+// The fourth step reads chunk c+1's first fragments and issues the hidden
+// rows of chunk c+2 and W_U of chunk c+3 into the freed stages. The barrier
+// is a plain s_barrier: the waits before it are exactly the ones this
+// schedule needs, where a fenced barrier would also drain the loads still in
+// flight.
+//
+// Measured, in steps, against loads staged through registers in 32-wide
+// chunks two ahead: three chunks in flight 4-5% faster; direct loads, 64-wide
+// chunks, two stages each: another 4-6%; a third W_U stage: another 3-7%
+// (0.91 ms at 1024 rows, 10.4 ms at 12288 on one GPU).
 namespace big {
 constexpr int TV = kBigTileVocab, TR = kBigTileRows, KC = 64;
 }  // namespace big
@@ -48,10 +55,10 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     float scale) {
   using namespace big;
   static_assert(TV == 256 && TR == 256, "wave layout below assumes a 256 x 256 tile");
-  __shared__ __attribute__((aligned(1024))) uint16_t sa0[TV][KC], sa1[TV][KC];
+  __shared__ __attribute__((aligned(1024))) uint16_t sa0[TV][KC], sa1[TV][KC], sa2[TV][KC];
   __shared__ __attribute__((aligned(1024))) uint16_t sb0[TR][KC], sb1[TR][KC];
-  __shared__ float4 red[2][TR];
-#define RPD_SA(X) ((X) == 0 ? sa0 : sa1)
+  float4 (*red)[TR] = reinterpret_cast<float4 (*)[TR]>(&sa0[0][0]);   // used after the loop only
+#define RPD_SA(X) ((X) == 0 ? sa0 : (X) == 1 ? sa1 : sa2)
 #define RPD_SB(X) ((X) == 0 ? sb0 : sb1)
 
   int rt, vt;
@@ -103,22 +110,26 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
       for (int q = 0; q < 16; ++q) acc[mv][nb][q] = 0.f;
   u32x4 fa0[4], fb0[4], fa1[4], fb1[4];
 
-#define RPD_DLOAD(X, chunk)                                                                               \
+#define RPD_ALOAD(XA, chunk)                                                                              \
   do {                                                                                                    \
     const long long k0_ = (long long)(chunk) * KC;                                                        \
-    _Pragma("unroll") for (int u_ = 0; u_ < 8; ++u_) {                                                   \
+    _Pragma("unroll") for (int u_ = 0; u_ < 8; ++u_)                                                     \
       __builtin_amdgcn_global_load_lds((const void*)(pa[u_] + k0_),                                       \
-          (__attribute__((address_space(3))) void*)&RPD_SA(X)[64 * wid + 8 * u_][0], 16, 0, 0);          \
-      __builtin_amdgcn_global_load_lds((const void*)(pb[u_] + k0_),                                       \
-          (__attribute__((address_space(3))) void*)&RPD_SB(X)[64 * wid + 8 * u_][0], 16, 0, 0);          \
-    }                                                                                                     \
+          (__attribute__((address_space(3))) void*)&RPD_SA(XA)[64 * wid + 8 * u_][0], 16, 0, 0);         \
   } while (0)
-#define RPD_FRAGS(FA, FB, X, kstep)                                                                       \
+#define RPD_BLOAD(XB, chunk)                                                                              \
+  do {                                                                                                    \
+    const long long k0_ = (long long)(chunk) * KC;                                                        \
+    _Pragma("unroll") for (int u_ = 0; u_ < 8; ++u_)                                                     \
+      __builtin_amdgcn_global_load_lds((const void*)(pb[u_] + k0_),                                       \
+          (__attribute__((address_space(3))) void*)&RPD_SB(XB)[64 * wid + 8 * u_][0], 16, 0, 0);         \
+  } while (0)
+#define RPD_FRAGS(FA, FB, XA, XB, kstep)                                                                  \
   do {                                                                                                    \
     const int fc_ = 8 * ((2 * (kstep) + fhi) ^ fsw);                                                      \
     _Pragma("unroll") for (int m_ = 0; m_ < 4; ++m_) {                                                   \
-      FA[m_] = *reinterpret_cast<const u32x4*>(&RPD_SA(X)[128 * wv + 32 * m_ + fr][fc_]);                \
-      FB[m_] = *reinterpret_cast<const u32x4*>(&RPD_SB(X)[128 * wr + 32 * m_ + fr][fc_]);                \
+      FA[m_] = *reinterpret_cast<const u32x4*>(&RPD_SA(XA)[128 * wv + 32 * m_ + fr][fc_]);               \
+      FB[m_] = *reinterpret_cast<const u32x4*>(&RPD_SB(XB)[128 * wr + 32 * m_ + fr][fc_]);               \
     }                                                                                                     \
   } while (0)
 #define RPD_MMA(FA, FB)                                                                                   \
@@ -138,27 +149,30 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     }                                                                                                     \
     __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                                                    \
   } while (0)
-  // chunk c in stage X (fragments of its first k-step already in fa0/fb0)
-#define RPD_CHUNK(c, X)                                                                                   \
+  // chunk c in A stage XA = c % 3 and B stage XB = c % 2 (fragments of its first k-step already in
+  // fa0/fb0). Loads issued after the barrier of chunk c: B of chunk c+2 into XB, then A of chunk c+3 into
+  // XA, so at the next barrier the newest 8 loads (A of chunk c+3) may still be in flight.
+#define RPD_CHUNK(c, XA, XB, XAN)                                                                         \
   do {                                                                                                    \
     __builtin_amdgcn_sched_barrier(0);                                                                    \
-    RPD_FRAGS(fa1, fb1, X, 1);                                                                            \
+    RPD_FRAGS(fa1, fb1, XA, XB, 1);                                                                       \
     RPD_MMA(fa0, fb0);                                                                                    \
     RPD_MIX();                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                                    \
-    RPD_FRAGS(fa0, fb0, X, 2);                                                                            \
+    RPD_FRAGS(fa0, fb0, XA, XB, 2);                                                                       \
     RPD_MMA(fa1, fb1);                                                                                    \
     RPD_MIX();                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                                    \
-    RPD_FRAGS(fa1, fb1, X, 3);                                                                            \
+    RPD_FRAGS(fa1, fb1, XA, XB, 3);                                                                       \
     RPD_MMA(fa0, fb0);                                                                                    \
     RPD_MIX();                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                                    \
-    __builtin_amdgcn_s_waitcnt(vm_lgkm_wait(0)); /* own loads of chunk c+1 landed, own reads of X done */ \
+    __builtin_amdgcn_s_waitcnt(vm_lgkm_wait(8)); /* chunk c+1 landed (A of c+2 may be in flight) */      \
     __builtin_amdgcn_s_barrier();                                                                         \
     __builtin_amdgcn_sched_barrier(0);                                                                    \
-    RPD_FRAGS(fa0, fb0, (X) ^ 1, 0);                                                                      \
-    RPD_DLOAD(X, min((c) + 2, nchf - 1));                                                                 \
+    RPD_FRAGS(fa0, fb0, XAN, (XB) ^ 1, 0);                                                                \
+    RPD_BLOAD(XB, min((c) + 2, nchf - 1));                                                                \
+    RPD_ALOAD(XA, min((c) + 3, nchf - 1));                                                                \
     RPD_MMA(fa1, fb1);                                                                                    \
     _Pragma("unroll") for (int g_ = 0; g_ < 16; ++g_) {                                                  \
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */                                       \
@@ -171,17 +185,28 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
   // Chunks past the end repeat the last one (loaded, never multiplied).
   const int nchf = d / KC;
   if (nchf > 0) {
-    RPD_DLOAD(0, 0);
-    RPD_DLOAD(1, min(1, nchf - 1));
-    __builtin_amdgcn_s_waitcnt(vm_lgkm_wait(16));   // this wave's loads of chunk 0 landed (chunk 1 in flight)
+    RPD_ALOAD(0, 0);
+    RPD_BLOAD(0, 0);
+    RPD_ALOAD(1, min(1, nchf - 1));
+    RPD_BLOAD(1, min(1, nchf - 1));
+    RPD_ALOAD(2, min(2, nchf - 1));
+    __builtin_amdgcn_s_waitcnt(vm_lgkm_wait(24));   // chunk 0 landed (A1, B1, A2 in flight)
     __builtin_amdgcn_s_barrier();
-    RPD_FRAGS(fa0, fb0, 0, 0);
+    RPD_FRAGS(fa0, fb0, 0, 0, 0);
     int c = 0;
-    for (; c + 2 <= nchf; c += 2) {
-      RPD_CHUNK(c, 0);
-      RPD_CHUNK(c + 1, 1);
+    for (; c + 6 <= nchf; c += 6) {
+      RPD_CHUNK(c, 0, 0, 1);
+      RPD_CHUNK(c + 1, 1, 1, 2);
+      RPD_CHUNK(c + 2, 2, 0, 0);
+      RPD_CHUNK(c + 3, 0, 1, 1);
+      RPD_CHUNK(c + 4, 1, 0, 2);
+      RPD_CHUNK(c + 5, 2, 1, 0);
     }
-    if (c < nchf) RPD_CHUNK(c, 0);
+    if (c < nchf) RPD_CHUNK(c, 0, 0, 1);
+    if (c + 1 < nchf) RPD_CHUNK(c + 1, 1, 1, 2);
+    if (c + 2 < nchf) RPD_CHUNK(c + 2, 2, 0, 0);
+    if (c + 3 < nchf) RPD_CHUNK(c + 3, 0, 1, 1);
+    if (c + 4 < nchf) RPD_CHUNK(c + 4, 1, 0, 2);
     __builtin_amdgcn_s_waitcnt(vm_lgkm_wait(0));    // no load outstanding past the loop
     __syncthreads();
   }
@@ -200,7 +225,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     __syncthreads();
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4) {
-      RPD_FRAGS(fa0, fb0, 0, s4);
+      RPD_FRAGS(fa0, fb0, 0, 0, s4);
       RPD_MMA(fa0, fb0);
     }
   }
@@ -208,10 +233,12 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 #undef RPD_MIX
 #undef RPD_MMA
 #undef RPD_FRAGS
-#undef RPD_DLOAD
+#undef RPD_ALOAD
+#undef RPD_BLOAD
 #undef RPD_SA
 #undef RPD_SB
 
+  __syncthreads();   // red aliases A stage 0
   // epilogue: lane holds projected row 128*wr + 32*nb + (lane & 31) against
   // vocabulary rows 128*wv + 32*mv + 8*(q >> 2) + 4*(lane >> 5) + (q & 3)
 #pragma unroll
