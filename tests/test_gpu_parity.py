@@ -69,6 +69,9 @@ BF16_CASES = [
     ("bf16_big_one_row_tile_odd_chunks", dict(B=1, L=80, K=3, d=200, V=6007, n_masked=80, masked_frac=None), 17),
     ("bf16_big_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
     ("bf16_big_row_split", dict(B=4, L=600, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
+    # the 256 x 256 tile with no full 64-wide chunk (only the zero-filled tail) and with exactly one
+    ("bf16_big_short_d", dict(B=1, L=80, K=3, d=56, V=3001, n_masked=80, masked_frac=None), 18),
+    ("bf16_big_one_chunk", dict(B=1, L=80, K=3, d=64, V=2011, n_masked=80, masked_frac=None), 19),
 ]
 
 
@@ -150,7 +153,9 @@ def test_fp32_normalization_and_scale():
 
 LAZY_CASES = [("bf16_s32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
               ("bf16_s128", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=16, masked_frac=None), 16),
-              ("bf16_big", dict(B=1, L=120, K=4, d=200, V=6007, n_masked=100, masked_frac=None), 17)]
+              ("bf16_big", dict(B=1, L=120, K=4, d=200, V=6007, n_masked=100, masked_frac=None), 17),
+              # 200 positions: the final-layer pass lists 200 rows, which the 256 x 256 tile takes
+              ("bf16_big_row_list", dict(B=1, L=240, K=4, d=136, V=3001, n_masked=200, masked_frac=None), 20)]
 
 
 @pytest.mark.parametrize("name,ov,seed", LAZY_CASES, ids=[c[0] for c in LAZY_CASES])
