@@ -295,6 +295,9 @@ def main() -> int:
                          "iteration until no position is masked (HIP-graph replays)")
     ap.add_argument("--sync-every", type=int, default=8,
                     help="--decode: iterations between read-backs of the masked count")
+    ap.add_argument("--cold", action="store_true",
+                    help="flush the last-level cache between calls with a 512 MB write (not timed: every call "
+                         "carries events and the value comes from the per-call times)")
     ap.add_argument("--event-every", type=int, default=4,
                     help="record the projection's HIP events on every N-th timed call (each event record "
                          "costs the stream a few microseconds)")
@@ -357,7 +360,8 @@ def main() -> int:
     torch.cuda.synchronize()
 
     K = args.steps
-    E = max(1, args.event_every)
+    E = 1 if args.cold else max(1, args.event_every)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev) if args.cold else None
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     proj_a = [ev() for _ in range((K + E - 1) // E)]
     proj_b = [ev() for _ in range((K + E - 1) // E)]
@@ -373,6 +377,8 @@ def main() -> int:
     t_wall0 = time.perf_counter()
     start.record()
     for k in range(K):
+        if flush is not None:
+            flush.fill_(k & 255)          # evicts W_U, hidden rows and outputs from the 256 MB cache
         if k % E == 0:
             j = k // E
             call(events=[call_a[j], proj_a[j], proj_b[j], None, call_b[j]])
@@ -383,6 +389,9 @@ def main() -> int:
     t_wall = time.perf_counter() - t_wall0
     ms_total = start.elapsed_time(end)
     ms_step = ms_total / K
+    if flush is not None:    # the flushes are in the loop: time the calls alone
+        ms_total = float(sum(a.elapsed_time(b) for a, b in zip(call_a, call_b)))
+        ms_step = ms_total / K
     proj_ms = [a.elapsed_time(b) for a, b in zip(proj_a, proj_b)]
     proj_avg = float(np.mean(proj_ms))
     call_ms = [a.elapsed_time(b) for a, b in zip(call_a, call_b)]
@@ -429,8 +438,10 @@ def main() -> int:
                    "masked_positions": n, "projected_rows": R, "seed": args.seed,
                    "commit_rule": "rpd_block" if P.block else "rpd", "final_norm": bool(args.norm),
                    "lazy_projection": bool(P.lazy),
-                   "cache_state": "W_U streamed from HBM every call (larger than the 256 MB last-level cache); "
-                                  "hidden rows, mask and outputs warm from the previous call"},
+                   "cache_state": ("cold: a 512 MB write between calls evicts everything; value from per-call "
+                                   "events" if args.cold else
+                                   "W_U streamed from HBM every call (larger than the 256 MB last-level cache); "
+                                   "hidden rows, mask and outputs warm from the previous call")},
         "iterations_per_s": round(1e3 / ms_step, 1),
         "call_us_sampled": pct(call_ms),
         "projection_us_sampled": pct(proj_ms),

@@ -138,17 +138,24 @@ __device__ __forceinline__ Soft soft_from_values(const float (&z)[N], const int 
 // dispatched round-robin over the 8 XCDs, so id % 8 selects the XCD and the
 // jobs of one XCD are laid out so that its concurrently running workgroups
 // share operands in that XCD's L2: with many row tiles each XCD owns a block
-// of row tiles and sweeps the vocabulary (all its tiles of one vocabulary
-// range run together); with few row tiles each XCD owns a contiguous range of
-// vocabulary tiles.
+// of row tiles and sweeps the vocabulary for groups of up to 8 of them (all
+// tiles of one vocabulary range and one group run together); with few row
+// tiles each XCD owns a contiguous range of vocabulary tiles.
 __device__ __forceinline__ bool map_job(int bid, int nvt, int nrt, int split_rows, int& rt, int& vt) {
   const int xcd = bid & 7, local = bid >> 3;
   if (split_rows) {
     const int lo = (int)((long long)xcd * nrt / 8), hi = (int)((long long)(xcd + 1) * nrt / 8);
     const int nr = hi - lo;
     if (nr <= 0 || local >= nr * nvt) return false;
-    vt = local / nr;
-    rt = lo + (local - vt * nr);
+    // the XCD's row tiles in groups of at most kRowGroup: a group's hidden rows stay cached while the
+    // vocabulary streams past once per group (with more row tiles than that, sweeping the vocabulary
+    // for all of them at once would re-read their hidden rows from HBM for every vocabulary tile)
+    constexpr int kRowGroup = 8;
+    const int g0 = local / (kRowGroup * nvt) * kRowGroup;
+    const int gsz = min(kRowGroup, nr - g0);
+    const int rem = local - g0 * nvt;
+    vt = rem / gsz;
+    rt = lo + g0 + (rem - vt * gsz);
   } else {
     const int lo = (int)((long long)xcd * nvt / 8), hi = (int)((long long)(xcd + 1) * nvt / 8);
     const int nv = hi - lo;

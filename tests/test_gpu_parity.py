@@ -72,6 +72,8 @@ BF16_CASES = [
     # the 256 x 256 tile with no full 64-wide chunk (only the zero-filled tail) and with exactly one
     ("bf16_big_short_d", dict(B=1, L=80, K=3, d=56, V=3001, n_masked=80, masked_frac=None), 18),
     ("bf16_big_one_chunk", dict(B=1, L=80, K=3, d=64, V=2011, n_masked=80, masked_frac=None), 19),
+    # 80 row tiles: 10 per XCD, swept in a group of 8 and a group of 2
+    ("bf16_big_row_groups", dict(B=64, L=80, K=4, d=64, V=700, n_masked=None, masked_frac=1.0), 21),
 ]
 
 
