@@ -85,8 +85,14 @@ __device__ int compact_in_workgroup(const CompactArgs& ca, int* s_pos, int need,
 // the 256 x 256 MFMA tile is faster.
 //
 // FC: the workgroup compacts the mask itself (compact_in_workgroup).
+//
+// Occupancy: the 4-wave forms run two workgroups per CU, which doubles the
+// W_U bytes in flight per CU (what the streaming rate depends on). The
+// 64-row form needs the launch bound's second argument for that (left to
+// itself the compiler took 185 VGPRs + 80 AGPRs, one workgroup per CU):
+// 4% faster at 64 rows. The 8-wave forms hold one workgroup per CU.
 template <int NW, int MV, int NB, bool FC>
-__global__ __launch_bounds__(NW * 64) void k_proj_bf16_stream(
+__global__ __launch_bounds__(NW * 64, (NW == 4 && NB >= 2) ? 2 : 1) void k_proj_bf16_stream(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
     int nvt, int nrt, int split_rows, CompactArgs ca, const uint16_t* __restrict__ xrows,
