@@ -255,8 +255,10 @@ enum {
   RPD_PROJ_BF16_S64 = 1,  /* bf16, 33..64 rows, same kernel family */
   RPD_PROJ_BF16_S128 = 2, /* bf16, 65..128 rows */
   RPD_PROJ_F32 = 3,       /* fp32 inputs, any row count */
-  RPD_PROJ_BF16_BIG = 4,  /* bf16, more than 192 rows: MFMA-bound 256 x 256 tiles */
-  RPD_PROJ_BF16_S192 = 5  /* bf16, 129..192 rows */
+  RPD_PROJ_BF16_BIG = 4,  /* bf16, more than 128 rows: MFMA tiles of 256 x 256 */
+  /* 5: no longer planned (a 129..192-row streaming form, replaced by 6) */
+  RPD_PROJ_BF16_BIG192 = 6 /* bf16, more than 128 rows where 256 x 192 tiles pad the rows less (129..192 rows
+                              always; above, whenever ceil(R/192)*192 < ceil(R/256)*256) */
 };
 
 /*

@@ -1,14 +1,16 @@
-// K1 projection, bf16, large row counts (more than 192 projected rows): the
-// MFMA-bound regime.
+// K1 projection, bf16, more than 128 projected rows: the MFMA-bound regime
+// (and the approach to it).
 #include "rpd_device.h"
 
 namespace rpd {
 namespace {
 
-// A GEMM tile of 256 vocabulary rows x 256 projected rows over the full
-// hidden dimension, four waves in a 2 x 2 layout, each computing 128 x 128
-// with v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane in AGPRs,
-// one wave per SIMD).
+// A GEMM tile of 256 vocabulary rows x TR projected rows (TR = 256 or 192)
+// over the full hidden dimension, four waves in a 2 x 2 layout, each computing
+// 128 x TR/2 with v_mfma_f32_32x32x16_bf16 (up to 256 fp32 accumulators per
+// lane in AGPRs, one wave per SIMD). The plan takes whichever row count pads
+// the projected rows less (192 rows measured 18% faster at 576 rows, where
+// 256-row tiles do a third more MFMA work).
 //
 // Operands go from global memory straight into LDS (global_load_lds_dwordx4:
 // each instruction deposits 64 lanes x 16 B = 8 rows x 128 B of one operand
@@ -20,8 +22,9 @@ namespace {
 // belongs at its LDS slot), which keeps the fragment reads free of bank
 // conflicts.
 //
-// Stages: three for W_U (32 KB each) and two for the hidden rows, which is
-// all 160 KB of LDS (the epilogue's reduction array reuses W_U stage 0). A
+// Stages: three for W_U (32 KB each) and two for the hidden rows (TR x 128 B
+// each): all 160 KB of LDS at TR = 256 (the epilogue's reduction array reuses
+// W_U stage 0). A
 // W_U chunk is first fetched from HBM by whichever of the workgroups sharing
 // it gets there first, while hidden rows mostly come from L2 or the MALL, so
 // W_U loads are issued two chunks earlier than hidden-row loads.
@@ -42,19 +45,22 @@ namespace {
 // chunks, two stages each: another 4-6%; a third W_U stage: another 3-7%
 // (0.91 ms at 1024 rows, 10.4 ms at 12288 on one GPU).
 namespace big {
-constexpr int TV = kBigTileVocab, TR = kBigTileRows, KC = 64;
+constexpr int TV = kBigTileVocab, KC = 64;
 }  // namespace big
 
 // s_waitcnt immediate: vmcnt <= n, lgkmcnt == 0, expcnt unconstrained
 constexpr unsigned vm_lgkm_wait(int n) { return (unsigned)((n & 15) | ((n >> 4) << 14) | (7 << 4)); }
 
+template <int TR>
 __global__ __launch_bounds__(256) void k_proj_bf16_big(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
     int nvt, int nrt, int split_rows, const uint16_t* __restrict__ xrows, const long long* __restrict__ rowoff,
     float scale) {
   using namespace big;
-  static_assert(TV == 256 && TR == 256, "wave layout below assumes a 256 x 256 tile");
+  static_assert(TV == 256 && (TR == 256 || TR == 192), "wave layout below assumes 256 x 256 or 256 x 192");
+  constexpr int NB = TR / 64;   // 32-row fragment blocks of the hidden rows per wave
+  constexpr int BL = TR / 32;   // hidden-row load instructions per wave per chunk
   __shared__ __attribute__((aligned(1024))) uint16_t sa0[TV][KC], sa1[TV][KC], sa2[TV][KC];
   __shared__ __attribute__((aligned(1024))) uint16_t sb0[TR][KC], sb1[TR][KC];
   float4 (*red)[TR] = reinterpret_cast<float4 (*)[TR]>(&sa0[0][0]);   // used after the loop only
@@ -71,19 +77,25 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wv = wid & 1, wr = wid >> 1;
 
-  // load sources: instruction u of this wave covers tile rows 64*wid + 8*u ..
-  // +8; lane l lands at LDS piece (l & 7) of row (l >> 3) and fetches the
-  // global piece (l & 7) ^ swizzle(row). Rows past the tile re-read its last
-  // vocabulary row, rows past the last projected row re-read row r0 (both
-  // discarded at the end).
+  // load sources: W_U instruction u of this wave covers tile rows 64*wid + 8*u
+  // .. +8, hidden-row instruction u rows (TR/4)*wid + 8*u .. +8; lane l lands
+  // at LDS piece (l & 7) of row (l >> 3) and fetches the global piece
+  // (l & 7) ^ swizzle(row). Rows past the tile re-read its last vocabulary
+  // row, rows past the last projected row re-read row r0 (both discarded at
+  // the end).
   const uint16_t* pa[8];
-  const uint16_t* pb[8];
+  const uint16_t* pb[BL];
   const uint16_t* __restrict__ xsrc = xrows ? xrows : hidden;
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     const int tr = 64 * wid + 8 * u + (lane >> 3);
     const int piece = (lane & 7) ^ ((tr >> 1) & 7);
     pa[u] = w_u + (long long)min(vb + tr, ve - 1) * d + piece * 8;
+  }
+#pragma unroll
+  for (int u = 0; u < BL; ++u) {
+    const int tr = (TR / 4) * wid + 8 * u + (lane >> 3);
+    const int piece = (lane & 7) ^ ((tr >> 1) & 7);
     const int r = r0 + tr < R ? r0 + tr : r0;
     long long ob;
     if (xrows) {   // normalized rows, already in projected-row order
@@ -101,14 +113,14 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
   // fragment reads: lane reads row base + (lane & 31), logical piece 2s + (lane >> 5)
   const int fr = lane & 31, fsw = (fr >> 1) & 7, fhi = lane >> 5;
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][NB];
 #pragma unroll
   for (int mv = 0; mv < 4; ++mv)
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[mv][nb][q] = 0.f;
-  u32x4 fa0[4], fb0[4], fa1[4], fb1[4];
+  u32x4 fa0[4], fb0[NB], fa1[4], fb1[NB];
 
 #define RPD_ALOAD(XA, chunk)                                                                              \
   do {                                                                                                    \
@@ -120,34 +132,33 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 #define RPD_BLOAD(XB, chunk)                                                                              \
   do {                                                                                                    \
     const long long k0_ = (long long)(chunk) * KC;                                                        \
-    _Pragma("unroll") for (int u_ = 0; u_ < 8; ++u_)                                                     \
+    _Pragma("unroll") for (int u_ = 0; u_ < BL; ++u_)                                                    \
       __builtin_amdgcn_global_load_lds((const void*)(pb[u_] + k0_),                                       \
-          (__attribute__((address_space(3))) void*)&RPD_SB(XB)[64 * wid + 8 * u_][0], 16, 0, 0);         \
+          (__attribute__((address_space(3))) void*)&RPD_SB(XB)[(TR / 4) * wid + 8 * u_][0], 16, 0, 0);   \
   } while (0)
 #define RPD_FRAGS(FA, FB, XA, XB, kstep)                                                                  \
   do {                                                                                                    \
     const int fc_ = 8 * ((2 * (kstep) + fhi) ^ fsw);                                                      \
-    _Pragma("unroll") for (int m_ = 0; m_ < 4; ++m_) {                                                   \
+    _Pragma("unroll") for (int m_ = 0; m_ < 4; ++m_)                                                     \
       FA[m_] = *reinterpret_cast<const u32x4*>(&RPD_SA(XA)[128 * wv + 32 * m_ + fr][fc_]);               \
-      FB[m_] = *reinterpret_cast<const u32x4*>(&RPD_SB(XB)[128 * wr + 32 * m_ + fr][fc_]);               \
-    }                                                                                                     \
+    _Pragma("unroll") for (int m_ = 0; m_ < NB; ++m_)                                                    \
+      FB[m_] = *reinterpret_cast<const u32x4*>(&RPD_SB(XB)[(TR / 2) * wr + 32 * m_ + fr][fc_]);          \
   } while (0)
 #define RPD_MMA(FA, FB)                                                                                   \
   do {                                                                                                    \
     _Pragma("unroll") for (int mv_ = 0; mv_ < 4; ++mv_)                                                  \
-    _Pragma("unroll") for (int nb_ = 0; nb_ < 4; ++nb_)                                                  \
+    _Pragma("unroll") for (int nb_ = 0; nb_ < NB; ++nb_)                                                 \
       acc[mv_][nb_] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, FA[mv_]),        \
                                                                __builtin_bit_cast(bf16x8, FB[nb_]),        \
                                                                acc[mv_][nb_], 0, 0, 0);                   \
   } while (0)
-  // 16 MFMAs with the 8 fragment reads of the next k-step between the first eight
+  // the 4*NB MFMAs of a k-step with the 4 + NB fragment reads of the next one between the first of them
 #define RPD_MIX()                                                                                         \
   do {                                                                                                    \
-    _Pragma("unroll") for (int g_ = 0; g_ < 8; ++g_) {                                                   \
+    _Pragma("unroll") for (int g_ = 0; g_ < 4 * NB; ++g_) {                                              \
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */                                       \
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* LDS read */                                   \
+      if (g_ < 4 + NB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* LDS read */                  \
     }                                                                                                     \
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                                                    \
   } while (0)
   // chunk c in A stage XA = c % 3 and B stage XB = c % 2 (fragments of its first k-step already in
   // fa0/fb0). Loads issued after the barrier of chunk c: B of chunk c+2 into XB, then A of chunk c+3 into
@@ -174,9 +185,9 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     RPD_BLOAD(XB, min((c) + 2, nchf - 1));                                                                \
     RPD_ALOAD(XA, min((c) + 3, nchf - 1));                                                                \
     RPD_MMA(fa1, fb1);                                                                                    \
-    _Pragma("unroll") for (int g_ = 0; g_ < 16; ++g_) {                                                  \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */                                       \
-      if (g_ < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* LDS read */                       \
+    _Pragma("unroll") for (int g_ = 0; g_ < 8 + BL; ++g_) {                                              \
+      if (g_ < 4 * NB) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */                      \
+      if (g_ < 4 + NB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* LDS read */                  \
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0); /* global->LDS load */                           \
     }                                                                                                     \
     __builtin_amdgcn_sched_barrier(0);                                                                    \
@@ -190,7 +201,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     RPD_ALOAD(1, min(1, nchf - 1));
     RPD_BLOAD(1, min(1, nchf - 1));
     RPD_ALOAD(2, min(2, nchf - 1));
-    __builtin_amdgcn_s_waitcnt(vm_lgkm_wait(24));   // chunk 0 landed (A1, B1, A2 in flight)
+    __builtin_amdgcn_s_waitcnt(vm_lgkm_wait(16 + BL));   // chunk 0 landed (A1, B1, A2 in flight)
     __builtin_amdgcn_s_barrier();
     RPD_FRAGS(fa0, fb0, 0, 0, 0);
     int c = 0;
@@ -218,8 +229,14 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
       const int piece = (lane & 7) ^ ((tr >> 1) & 7);
       const bool in = k0 + piece * 8 < d;
       const u32x4 va = in ? *reinterpret_cast<const u32x4*>(pa[u] + k0) : u32x4{0u, 0u, 0u, 0u};
-      const u32x4 vh = in ? *reinterpret_cast<const u32x4*>(pb[u] + k0) : u32x4{0u, 0u, 0u, 0u};
       *reinterpret_cast<u32x4*>(&sa0[tr][(lane & 7) * 8]) = va;
+    }
+#pragma unroll
+    for (int u = 0; u < BL; ++u) {
+      const int tr = (TR / 4) * wid + 8 * u + (lane >> 3);
+      const int piece = (lane & 7) ^ ((tr >> 1) & 7);
+      const bool in = k0 + piece * 8 < d;
+      const u32x4 vh = in ? *reinterpret_cast<const u32x4*>(pb[u] + k0) : u32x4{0u, 0u, 0u, 0u};
       *reinterpret_cast<u32x4*>(&sb0[tr][(lane & 7) * 8]) = vh;
     }
     __syncthreads();
@@ -239,10 +256,10 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 #undef RPD_SB
 
   __syncthreads();   // red aliases A stage 0
-  // epilogue: lane holds projected row 128*wr + 32*nb + (lane & 31) against
+  // epilogue: lane holds projected row (TR/2)*wr + 32*nb + (lane & 31) against
   // vocabulary rows 128*wv + 32*mv + 8*(q >> 2) + 4*(lane >> 5) + (q & 3)
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) {
+  for (int nb = 0; nb < NB; ++nb) {
     Soft sst = soft_empty();
 #pragma unroll
     for (int mv = 0; mv < 4; ++mv) {
@@ -259,11 +276,11 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
       sst = soft_merge(sst, soft_from_values(z, vi, ok));
     }
     sst = soft_merge(sst, soft_shfl_xor(sst, 32));
-    if (lane < 32) red[wv][128 * wr + 32 * nb + lane] = soft_pack(sst);
+    if (lane < 32) red[wv][(TR / 2) * wr + 32 * nb + lane] = soft_pack(sst);
   }
   __syncthreads();
-  {
-    const int r = r0 + tid;   // one projected row per thread (TR == 256 threads)
+  if (tid < TR) {   // one projected row per thread
+    const int r = r0 + tid;
     if (r < R) {
       const Soft sres = soft_merge(soft_unpack(red[0][tid]), soft_unpack(red[1][tid]));
       partials[(long long)r * nvt + vt] = soft_pack(sres);
@@ -274,7 +291,8 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 }  // namespace
 
 hipError_t launch_proj_big(const Launch& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_proj_bf16_big, dim3(a.plan.grid), dim3(256), 0, s, static_cast<const uint16_t*>(a.hidden),
+  auto kernel = a.plan.rows_per_tile == 192 ? k_proj_bf16_big<192> : k_proj_bf16_big<256>;
+  hipLaunchKernelGGL(kernel, dim3(a.plan.grid), dim3(256), 0, s, static_cast<const uint16_t*>(a.hidden),
                      static_cast<const uint16_t*>(a.w_u), a.rows, a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V,
                      a.plan.nvt, a.plan.nrt, a.plan.split_rows, static_cast<const uint16_t*>(a.xrows), a.rowoff,
                      a.logit_scale);

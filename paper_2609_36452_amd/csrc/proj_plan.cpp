@@ -22,18 +22,19 @@ ProjPlan plan_projection(int dtype, long long rows_cap, int V) {
     // HBM-bound: one row tile holding every projected row, so W_U is read
     // once; a multiple of 256 equal vocabulary tiles, so every CU streams the
     // same share
-    p.variant = rows_cap <= 32    ? PROJ_BF16_S32
-                : rows_cap <= 64  ? PROJ_BF16_S64
-                : rows_cap <= 128 ? PROJ_BF16_S128
-                                  : PROJ_BF16_S192;
-    p.rows_per_tile = rows_cap <= 32 ? 32 : rows_cap <= 64 ? 64 : rows_cap <= 128 ? 128 : 192;
+    p.variant = rows_cap <= 32 ? PROJ_BF16_S32 : rows_cap <= 64 ? PROJ_BF16_S64 : PROJ_BF16_S128;
+    p.rows_per_tile = rows_cap <= 32 ? 32 : rows_cap <= 64 ? 64 : 128;
     p.vocab_cap = kStreamTileVocab;
     int nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
     nvt = ((nvt + 255) / 256) * 256;
     p.nvt = nvt < V ? nvt : V;
   } else {
-    p.variant = PROJ_BF16_BIG;
-    p.rows_per_tile = kBigTileRows;
+    // MFMA tiles of 256 vocabulary rows x 256 or 192 projected rows, whichever
+    // pads the rows less (ties to 256)
+    const long long pad256 = (rows_cap + kBigTileRows - 1) / kBigTileRows * kBigTileRows;
+    const long long pad192 = (rows_cap + kBigTileRowsSmall - 1) / kBigTileRowsSmall * kBigTileRowsSmall;
+    p.variant = pad192 < pad256 ? PROJ_BF16_BIG192 : PROJ_BF16_BIG;
+    p.rows_per_tile = pad192 < pad256 ? kBigTileRowsSmall : kBigTileRows;
     p.vocab_cap = kBigTileVocab;
     p.nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
   }
@@ -49,9 +50,9 @@ hipError_t launch_projection(const Launch& a, hipStream_t s) {
   switch (a.plan.variant) {
     case PROJ_BF16_S32:
     case PROJ_BF16_S64:
-    case PROJ_BF16_S128:
-    case PROJ_BF16_S192: return launch_proj_stream(a, s);
-    case PROJ_BF16_BIG: return launch_proj_big(a, s);
+    case PROJ_BF16_S128: return launch_proj_stream(a, s);
+    case PROJ_BF16_BIG:
+    case PROJ_BF16_BIG192: return launch_proj_big(a, s);
     case PROJ_F32: return launch_proj_f32(a, s);
   }
   return hipErrorInvalidValue;

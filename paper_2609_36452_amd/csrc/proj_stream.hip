@@ -315,7 +315,7 @@ void launch_stream(const Launch& a, hipStream_t s) {
 
 bool compact_fused(const Launch& a) {
   const ProjVariant v = a.plan.variant;
-  const bool streaming = v == PROJ_BF16_S32 || v == PROJ_BF16_S64 || v == PROJ_BF16_S128 || v == PROJ_BF16_S192;
+  const bool streaming = v == PROJ_BF16_S32 || v == PROJ_BF16_S64 || v == PROJ_BF16_S128;
   return streaming && a.plan.nrt == 1 && a.max_masked > 0 && (long long)a.B * a.L <= kFusedCompactMax &&
          !a.xrows && !a.rowoff;   // the normalization and explicit row lists need the compaction first
 }
@@ -325,7 +325,6 @@ hipError_t launch_proj_stream(const Launch& a, hipStream_t s) {
     case PROJ_BF16_S32: launch_stream<4, 2, 1>(a, s); break;
     case PROJ_BF16_S64: launch_stream<4, 2, 2>(a, s); break;
     case PROJ_BF16_S128: launch_stream<8, 1, 4>(a, s); break;
-    case PROJ_BF16_S192: launch_stream<8, 1, 6>(a, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -16,17 +16,20 @@ enum ProjVariant {
   PROJ_BF16_S64 = 1,    // <= 64 rows, same kernel family
   PROJ_BF16_S128 = 2,   // <= 128 rows
   PROJ_F32 = 3,         // fp32 inputs: vector ALU, 16 rows x 64 vocab
-  PROJ_BF16_BIG = 4,    // > 192 rows, MFMA-bound: 256 x 256 tiles, both operands staged through LDS
-  PROJ_BF16_S192 = 5,   // <= 192 rows
+  PROJ_BF16_BIG = 4,    // MFMA-bound: 256 x 256 tiles, both operands staged through LDS
+  PROJ_BF16_BIG192 = 6, // the same kernel with 256 x 192 tiles (where they pad the rows less)
 };
 
 // tile of the large-row variant: vocabulary rows x projected rows
 constexpr int kBigTileVocab = 256, kBigTileRows = 256;
 // vocabulary rows of one workgroup of the streaming variants (all of them)
 constexpr int kStreamTileVocab = 256;
-// most projected rows a streaming variant takes; above, the 256 x 256 tile
-// is faster (measured at 224 and 256 rows at the LLaDA-8B shape)
-constexpr int kStreamMaxRows = 192;
+// most projected rows a streaming variant takes; above, the MFMA tiles are
+// faster (256 x 192 measured 3-8% faster than 192-row streaming at 132-192
+// rows, 256 x 256 7-9% faster than 256-row streaming at 224 and 256)
+constexpr int kStreamMaxRows = 128;
+// rows of the smaller MFMA tile
+constexpr int kBigTileRowsSmall = 192;
 // largest canvas (B * L) whose compaction the streaming projection does itself
 constexpr int kFusedCompactMax = 2048;
 
@@ -131,7 +134,7 @@ bool compact_fused(const Launch& a);
 // the projection variants, dispatched by launch_projection on a.plan.variant
 // the final normalization of the compacted rows into a.xrows (before the projection)
 hipError_t launch_norm_rows(const Launch& a, hipStream_t s);
-hipError_t launch_proj_stream(const Launch& a, hipStream_t s);  // PROJ_BF16_S32 .. PROJ_BF16_S192
+hipError_t launch_proj_stream(const Launch& a, hipStream_t s);  // PROJ_BF16_S32 .. PROJ_BF16_S128
 hipError_t launch_proj_big(const Launch& a, hipStream_t s);     // PROJ_BF16_BIG
 hipError_t launch_proj_f32(const Launch& a, hipStream_t s);     // PROJ_F32
 

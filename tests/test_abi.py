@@ -75,8 +75,10 @@ def test_workspace_size():
 def test_projection_variant_thresholds():
     pv = lambda n, dt=rpd.DTYPE_BF16: rpd.projection_variant(4, 1, 256, 4096, 126464, dt, max_masked=n)  # noqa: E731
     assert [pv(n) for n in (1, 8, 9, 16, 17, 32, 33, 48, 49, 64, 65, 256)] == \
-        ["bf16_s32", "bf16_s32", "bf16_s64", "bf16_s64", "bf16_s128", "bf16_s128", "bf16_s192", "bf16_s192",
-         "bf16_big", "bf16_big", "bf16_big", "bf16_big"]
+        ["bf16_s32", "bf16_s32", "bf16_s64", "bf16_s64", "bf16_s128", "bf16_s128", "bf16_big192", "bf16_big192",
+         "bf16_big", "bf16_big", "bf16_big192", "bf16_big"]
+    # above 128 rows: the MFMA tile of 192 or 256 rows that pads the rows less (ties to 256)
+    assert [pv(n) for n in (96, 144, 192, 225)] == ["bf16_big192", "bf16_big192", "bf16_big", "bf16_big192"]
     assert pv(8, rpd.DTYPE_F32) == "f32" and pv(256, rpd.DTYPE_F32) == "f32"
     assert pv(-1) == "bf16_big"          # -1 plans for every position masked
     with pytest.raises(rpd.RpdError):

@@ -65,10 +65,14 @@ BF16_CASES = [
     ("bf16_s32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
     ("bf16_s64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10, masked_frac=None), 12),
     ("bf16_s128_long_d", dict(B=1, L=40, K=4, d=4104, V=2500, n_masked=20, masked_frac=None), 15),
-    ("bf16_s192_two_seqs", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=20, masked_frac=None), 16),
+    ("bf16_big192_two_seqs", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=20, masked_frac=None), 16),
     ("bf16_big_one_row_tile_odd_chunks", dict(B=1, L=80, K=3, d=200, V=6007, n_masked=80, masked_frac=None), 17),
     ("bf16_big_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
-    ("bf16_big_row_split", dict(B=4, L=600, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
+    ("bf16_big192_row_split", dict(B=4, L=600, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
+    ("bf16_big_row_split", dict(B=4, L=512, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 22),
+    ("bf16_big192_three_row_tiles", dict(B=2, L=100, K=4, d=264, V=3001, n_masked=72, masked_frac=None), 23),
+    ("bf16_big192_short_d", dict(B=1, L=60, K=3, d=56, V=3001, n_masked=48, masked_frac=None), 24),
+    ("bf16_big192_one_chunk", dict(B=1, L=60, K=3, d=64, V=2011, n_masked=48, masked_frac=None), 25),
     # the 256 x 256 tile with no full 64-wide chunk (only the zero-filled tail) and with exactly one
     ("bf16_big_short_d", dict(B=1, L=80, K=3, d=56, V=3001, n_masked=80, masked_frac=None), 18),
     ("bf16_big_one_chunk", dict(B=1, L=80, K=3, d=64, V=2011, n_masked=80, masked_frac=None), 19),
