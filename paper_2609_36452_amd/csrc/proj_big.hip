@@ -12,10 +12,13 @@ namespace {
 // the projected rows less (192 rows measured 18% faster at 576 rows, where
 // 256-row tiles do a third more MFMA work).
 //
-// Operands go from global memory straight into LDS (global_load_lds_dwordx4:
-// each instruction deposits 64 lanes x 16 B = 8 rows x 128 B of one operand
-// at the LDS address in M0), in 64-wide k-chunks, and are read back as MFMA
-// fragments. No register staging and no LDS store instructions: with them,
+// Operands go from global memory straight into LDS (each load instruction
+// deposits 64 lanes x 16 B = 8 rows x 128 B of one operand at the LDS address
+// in M0), in 64-wide k-chunks, and are read back as MFMA fragments. W_U comes
+// through buffer loads (a resource at the tile's first row, fixed 32-bit lane
+// offsets, the chunk's offset in a scalar register: no per-load 64-bit address
+// arithmetic, 4% fewer loop cycles than global_load_lds with 64-bit lane
+// addresses); the gathered hidden rows through global_load_lds. No register staging and no LDS store instructions: with them,
 // the LDS instruction queue saturated (counters showed its data FIFO full
 // for 1.2e7 cycles per call at 1024 rows). The eight 16-byte pieces of row r
 // sit XOR-swizzled by (r >> 1) & 7 (each lane fetches the global piece that
@@ -53,7 +56,10 @@ constexpr int TV = kBigTileVocab, KC = 64;
 // s_waitcnt immediate: vmcnt <= n, lgkmcnt == 0, expcnt unconstrained
 constexpr unsigned vm_lgkm_wait(int n) { return (unsigned)((n & 15) | ((n >> 4) << 14) | (7 << 4)); }
 
-template <int TR>
+// NT: W_U loads non-temporal, for a single row tile (no other workgroup reads
+// the same W_U chunk: 11% faster at 256 rows; with several row tiles sharing
+// chunks through L2 it was 3% slower).
+template <int TR, bool NT>
 __global__ __launch_bounds__(256) void k_proj_bf16_big(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ n_ptr, float4* __restrict__ partials, int K, int B, int L, int d, int V,
@@ -85,14 +91,16 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
   // (l & 7) ^ swizzle(row). Rows past the tile re-read its last vocabulary
   // row, rows past the last projected row re-read row r0 (both discarded at
   // the end).
-  const uint16_t* pa[8];
+  int pa[8];   // byte offsets of this lane's pieces from the tile's first W_U row (< 256 * d * 2)
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(w_u + (long long)vb * d), (short)0, (ve - vb) * d * 2, 0x00020000);
   const uint16_t* pb[BL];
   const uint16_t* __restrict__ xsrc = xrows ? xrows : hidden;
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     const int tr = 64 * wid + 8 * u + (lane >> 3);
     const int piece = (lane & 7) ^ ((tr >> 1) & 7);
-    pa[u] = w_u + (long long)min(vb + tr, ve - 1) * d + piece * 8;
+    pa[u] = ((min(vb + tr, ve - 1) - vb) * d + piece * 8) * 2;
   }
 #pragma unroll
   for (int u = 0; u < BL; ++u) {
@@ -130,8 +138,9 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
   do {                                                                                                    \
     const long long k0_ = (long long)(chunk) * KC;                                                        \
     _Pragma("unroll") for (int u_ = (U0); u_ < (U1); ++u_)                                               \
-      __builtin_amdgcn_global_load_lds((const void*)(pa[u_] + k0_),                                       \
-          (__attribute__((address_space(3))) void*)&RPD_SA(XA)[64 * wid + 8 * u_][0], 16, 0, 0);         \
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs,                                                        \
+          (__attribute__((address_space(3))) void*)&RPD_SA(XA)[64 * wid + 8 * u_][0], 16, pa[u_],           \
+          (int)(2 * k0_), 0, NT ? 2 : 0);                                                                  \
   } while (0)
 #define RPD_BLOAD_R(XB, chunk, U0, U1)                                                                    \
   do {                                                                                                    \
@@ -239,7 +248,8 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
       const int tr = 64 * wid + 8 * u + (lane >> 3);
       const int piece = (lane & 7) ^ ((tr >> 1) & 7);
       const bool in = k0 + piece * 8 < d;
-      const u32x4 va = in ? *reinterpret_cast<const u32x4*>(pa[u] + k0) : u32x4{0u, 0u, 0u, 0u};
+      const u32x4 va = in ? *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(w_u + (long long)vb * d) + 2 * k0 + pa[u])
+                          : u32x4{0u, 0u, 0u, 0u};
       *reinterpret_cast<u32x4*>(&sa0[tr][(lane & 7) * 8]) = va;
     }
 #pragma unroll
@@ -349,7 +359,9 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 }  // namespace
 
 hipError_t launch_proj_big(const Launch& a, hipStream_t s) {
-  auto kernel = a.plan.rows_per_tile == 192 ? k_proj_bf16_big<192> : k_proj_bf16_big<256>;
+  const bool nt = a.plan.nrt == 1;
+  auto kernel = a.plan.rows_per_tile == 192 ? (nt ? k_proj_bf16_big<192, true> : k_proj_bf16_big<192, false>)
+                                            : (nt ? k_proj_bf16_big<256, true> : k_proj_bf16_big<256, false>);
   hipLaunchKernelGGL(kernel, dim3(a.plan.grid), dim3(256), 0, s, static_cast<const uint16_t*>(a.hidden),
                      static_cast<const uint16_t*>(a.w_u), a.rows, a.n_masked, a.partials, a.K, a.B, a.L, a.d, a.V,
                      a.plan.nvt, a.plan.nrt, a.plan.split_rows, static_cast<const uint16_t*>(a.xrows), a.rowoff,
