@@ -3,9 +3,10 @@
 Small and mid-size cases are compared element by element (every masked
 position, every layer); they span several vocabulary and row tiles, ragged
 vocabulary sizes and hidden sizes that are not multiples of the 64-wide
-k-chunk, and every projection variant (the streaming family at <= 32, 64,
-128, 192 and 256 projected rows, and the MFMA tile above, with row tiles
-split across XCDs). Full-size LLaDA-8B / Dream-7B shapes are
+k-chunk, and every projection variant (the streaming family at <= 32, 64
+and 128 projected rows, and the 192- and 256-row MFMA tiles above, with row
+tiles split across XCDs, and rows gathered through 32-bit buffer offsets or,
+from a hidden tensor of more than 2^31 bytes, 64-bit addresses). Full-size LLaDA-8B / Dream-7B shapes are
 compared on sampled positions that the oracle computes one by one, plus the
 prefix-sum identity of the commitment on the GPU's own outputs."""
 import dataclasses
@@ -309,6 +310,43 @@ def test_gate_commit_matches_oracle_selection(block):
         np.testing.assert_allclose(g["upstream_entropy"][b][m[b]], o["upstream_entropy"][b][m[b]], atol=1e-4)
         assert g["n_commit"][b] == o["n_commit"][b]
     assert (g["token"][~m] == -1).all() and (g["commit"][~m] == 0).all()
+
+
+@pytest.mark.parametrize("n", [64, 72])
+def test_big_tile_wide_row_offsets(n):
+    # With more than 2^31 bytes of hidden states the big tile gathers rows through 64-bit addresses
+    # instead of 32-bit buffer offsets. The same rows at the same relative order in a small canvas take
+    # the buffer path: every output at the masked positions must agree bit for bit (and the small
+    # canvas agrees with the oracle). n = 64: one 256-row tile; 72: two 192-row tiles.
+    cfg = CONFIGS["llada_late"].with_(name=f"wide{n}", B=1, L=n, K=4, d=4096, V=3001, n_masked=n,
+                                      masked_frac=None)
+    w = make_workload(cfg, 40 + n)
+    P = O.strict(4, 1.0)
+    g_small, _, _ = _check(w, P)
+    Lbig = 65600   # 4 layers x 65600 x 4096 bf16 = 2.15 GB
+    assert 4 * Lbig * 4096 * 2 > 2 ** 31
+    pos = torch.arange(n, device="cuda:0") * 911 + 17   # increasing, spread over the canvas
+    assert int(pos[-1]) < Lbig
+    hidden_s, w_u, _ = to_device(w)
+    hidden = torch.zeros((4, 1, Lbig, 4096), dtype=torch.bfloat16, device="cuda:0")
+    hidden[:, 0, pos] = hidden_s[:, 0, :]
+    mask = torch.zeros((1, Lbig), dtype=torch.uint8, device="cuda:0")
+    mask[0, pos] = 1
+    variant = rpd.projection_variant(4, 1, Lbig, 4096, 3001, hidden.dtype, max_masked=n)
+    note(f"  wide canvas L={Lbig}, {n} masked, variant {variant}")
+    assert variant == ("bf16_big" if n == 64 else "bf16_big192")
+    out = rpd.score_commit(hidden, w_u, mask, gpu_params(P), max_masked=n, layer_stats=True)
+    torch.cuda.synchronize()
+    pc = pos.cpu().numpy()
+    for k, v in out.items():
+        a = v.cpu().numpy()
+        b = g_small[k]
+        if a.shape[-1] == Lbig:
+            a = a[..., pc]
+        assert a.shape == b.shape, k
+        assert np.array_equal(np.ascontiguousarray(a).view(np.uint8), np.ascontiguousarray(b).view(np.uint8)), k
+    del hidden, out
+    torch.cuda.empty_cache()
 
 
 # -------------------------------------------------------------- full size --
