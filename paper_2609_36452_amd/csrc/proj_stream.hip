@@ -68,6 +68,14 @@ __device__ int compact_in_workgroup(const CompactArgs& ca, int* s_pos, int need,
 // neither a second stage nor a barrier: one wave's LDS accesses complete in
 // program order.
 //
+// Chunk order: workgroup tile vt takes the full chunks starting at
+// (7 * vt) mod (d / 64) and wrapping around. In plain order every workgroup
+// reads the same 128-byte column of rows 8 KB apart at the same time, so the
+// low 13 address bits of all requests in flight match and they crowd onto
+// a few HBM channels: a read probe of that order reached 5.7-5.9 TB/s where
+// linear reads reach 7.0, and rotated starts 6.9 (the spread between boxes
+// came mostly from this).
+//
 // Hidden rows: the TR rows of chunk c are loaded cooperatively by all
 // threads (same line layout and swizzle) into one of two workgroup-shared
 // LDS stages; one barrier per chunk publishes it, and the stage is refilled
@@ -131,6 +139,9 @@ __global__ __launch_bounds__(NW * 64, (NW == 4 && NB >= 2) ? 2 : 1) void k_proj_
   u32x4 ld[D][NLD];
   u32x4 xr[D][XLD];
   const int nchf = d / KC;
+  // full chunks are taken in the order rot, rot+1, .., nchf-1, 0, .., rot-1
+  const int rot = nchf > 0 ? (int)((7ll * vt) % nchf) : 0;
+#define RPD_PCHUNK(c) ((c) + rot >= nchf ? (c) + rot - nchf : (c) + rot)
   // W_U loads of the first two chunks go out before anything waits
   if (has_job && nchf > 0) {
 #pragma unroll
@@ -138,7 +149,7 @@ __global__ __launch_bounds__(NW * 64, (NW == 4 && NB >= 2) ? 2 : 1) void k_proj_
 #pragma unroll
       for (int u = 0; u < NLD; ++u)
         ld[j][u] = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(w_u + wa[u] + (long long)min(j, nchf - 1) * KC));
+            reinterpret_cast<const u32x4*>(w_u + wa[u] + (long long)RPD_PCHUNK(min(j, nchf - 1)) * KC));
   }
   int R;
   if (FC) {
@@ -186,13 +197,13 @@ __global__ __launch_bounds__(NW * 64, (NW == 4 && NB >= 2) ? 2 : 1) void k_proj_
       for (int q = 0; q < 16; ++q) acc[mv][nb][q] = 0.f;
 #define RPD_XLOAD(slot, chunk)                                                                           \
   do {                                                                                                   \
-    const long long k0_ = (long long)(chunk) * KC;                                                       \
+    const long long k0_ = (long long)RPD_PCHUNK(chunk) * KC;                                             \
     _Pragma("unroll") for (int u_ = 0; u_ < XLD; ++u_)                                                  \
       xr[slot][u_] = *reinterpret_cast<const u32x4*>(xsrc + xa[u_] + k0_);                               \
   } while (0)
 #define RPD_SLOAD(slot, chunk)                                                                           \
   do {                                                                                                   \
-    const long long k0_ = (long long)(chunk) * KC;                                                       \
+    const long long k0_ = (long long)RPD_PCHUNK(chunk) * KC;                                             \
     _Pragma("unroll") for (int u_ = 0; u_ < NLD; ++u_)                                                  \
       ld[slot][u_] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(w_u + wa[u_] + k0_));     \
     RPD_XLOAD(slot, chunk);                                                                              \
@@ -257,6 +268,7 @@ __global__ __launch_bounds__(NW * 64, (NW == 4 && NB >= 2) ? 2 : 1) void k_proj_
   }
 #undef RPD_SCHUNK
 #undef RPD_SMMA
+#undef RPD_PCHUNK
 #undef RPD_SLOAD
 #undef RPD_XLOAD
 
