@@ -146,7 +146,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 #define RPD_BLOAD(XB, chunk) RPD_BLOAD_R(XB, chunk, 0, BL)
 #define RPD_ALOAD_R(XA, chunk, U0, U1)                                                                    \
   do {                                                                                                    \
-    const long long k0_ = (long long)(chunk) * KC;                                                        \
+    const long long k0_ = (long long)RPD_PCHUNK(chunk) * KC;                                              \
     _Pragma("unroll") for (int u_ = (U0); u_ < (U1); ++u_)                                               \
       __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs,                                                        \
           (__attribute__((address_space(3))) void*)&RPD_SA(XA)[64 * wid + 8 * u_][0], 16, pa[u_],           \
@@ -154,7 +154,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
   } while (0)
 #define RPD_BLOAD_R(XB, chunk, U0, U1)                                                                    \
   do {                                                                                                    \
-    const long long k0_ = (long long)(chunk) * KC;                                                        \
+    const long long k0_ = (long long)RPD_PCHUNK(chunk) * KC;                                              \
     _Pragma("unroll") for (int u_ = (U0); u_ < (U1); ++u_)                                               \
       if constexpr (HB)                                                                                   \
         __builtin_amdgcn_raw_ptr_buffer_load_lds(hrs,                                                      \
@@ -227,8 +227,16 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     __builtin_amdgcn_sched_barrier(0);                                                                    \
   } while (0)
 
-  // Chunks past the end repeat the last one (loaded, never multiplied).
+  // Chunks past the end repeat the last one (loaded, never multiplied). With a
+  // single row tile (NT) full chunks are taken in the order rot, rot+1, ..,
+  // nchf-1, 0, .., rot-1: requests in flight on different vocabulary tiles
+  // then read different columns of W_U (in plain order they crowded onto a
+  // few HBM channels). With several row tiles the plain order stays: the
+  // workgroups of one row tile share its hidden rows through L2 only while
+  // they read the same chunk (rotated, 7-8% slower at 1024 rows and up).
   const int nchf = d / KC;
+  const int rot = NT && nchf > 0 ? (int)((7ll * vt) % nchf) : 0;
+#define RPD_PCHUNK(c) ((c) + rot >= nchf ? (c) + rot - nchf : (c) + rot)
   if (nchf > 0) {
     RPD_ALOAD(0, 0);
     RPD_BLOAD(0, 0);
@@ -289,6 +297,7 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 #undef RPD_ALOAD
 #undef RPD_BLOAD
 #undef RPD_ALOAD_R
+#undef RPD_PCHUNK
 #undef RPD_BLOAD_R
 #undef RPD_SA
 #undef RPD_SB
