@@ -31,11 +31,12 @@ METRIC = "masked positions scored+committed/sec at LLaDA-8B shape; MFMA % / HBM 
 CSRC = os.path.join(ROOT, "paper_2609_36452_amd", "csrc")
 # the source files that define each projection variant's kernel
 VARIANT_SOURCES = {v: ["rpd_device.h", "proj_stream.hip"] for v in
-                   ("bf16_s32", "bf16_s64", "bf16_s128")}
-VARIANT_SOURCES.update({"bf16_big": ["rpd_device.h", "proj_big.hip"], "bf16_big192": ["rpd_device.h", "proj_big.hip"],
-                        "f32": ["rpd_device.h", "proj_f32.hip"]})
-VARIANT_KERNEL = {v: "k_proj_bf16_stream" for v in ("bf16_s32", "bf16_s64", "bf16_s128")}
-VARIANT_KERNEL.update({"bf16_big": "k_proj_bf16_big", "bf16_big192": "k_proj_bf16_big", "f32": "k_proj_f32"})
+                   ("bf16_s32", "bf16_s64")}
+VARIANT_SOURCES.update({v: ["rpd_device.h", "proj_big.hip"] for v in ("bf16_big", "bf16_big192", "bf16_big128")})
+VARIANT_SOURCES["f32"] = ["rpd_device.h", "proj_f32.hip"]
+VARIANT_KERNEL = {v: "k_proj_bf16_stream" for v in ("bf16_s32", "bf16_s64")}
+VARIANT_KERNEL.update({v: "k_proj_bf16_big" for v in ("bf16_big", "bf16_big192", "bf16_big128")})
+VARIANT_KERNEL["f32"] = "k_proj_f32"
 COPY_PROBE_BYTES = 1 << 30     # fp32 elements read (and as many written) by the copy probe
 
 

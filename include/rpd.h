@@ -253,12 +253,13 @@ rpd_status rpd_gate_commit(int32_t K, int32_t B, int32_t L, const uint8_t* mask,
 enum {
   RPD_PROJ_BF16_S32 = 0,  /* bf16, at most 32 projected rows: W_U streamed once from HBM */
   RPD_PROJ_BF16_S64 = 1,  /* bf16, 33..64 rows, same kernel family */
-  RPD_PROJ_BF16_S128 = 2, /* bf16, 65..128 rows */
+  /* 2: no longer planned (a 65..128-row streaming form, replaced by 7) */
   RPD_PROJ_F32 = 3,       /* fp32 inputs, any row count */
   RPD_PROJ_BF16_BIG = 4,  /* bf16, more than 128 rows: MFMA tiles of 256 x 256 */
   /* 5: no longer planned (a 129..192-row streaming form, replaced by 6) */
-  RPD_PROJ_BF16_BIG192 = 6 /* bf16, more than 128 rows where 256 x 192 tiles pad the rows less (129..192 rows
-                              always; above, whenever ceil(R/192)*192 < ceil(R/256)*256) */
+  RPD_PROJ_BF16_BIG192 = 6, /* bf16, more than 128 rows where 256 x 192 tiles pad the rows less (129..192 rows
+                               always; above, whenever ceil(R/192)*192 < ceil(R/256)*256) */
+  RPD_PROJ_BF16_BIG128 = 7  /* bf16, 65..128 rows: one MFMA tile of 256 x 128 per vocabulary tile */
 };
 
 /*

@@ -177,7 +177,7 @@ def workspace_size(K: int, B: int, L: int, d: int, V: int, dtype: torch.dtype | 
     return int(lib().rpd_workspace_size(ctypes.byref(p)))
 
 
-PROJ_VARIANTS = {0: "bf16_s32", 1: "bf16_s64", 2: "bf16_s128", 3: "f32", 4: "bf16_big", 6: "bf16_big192"}
+PROJ_VARIANTS = {0: "bf16_s32", 1: "bf16_s64", 3: "f32", 4: "bf16_big", 6: "bf16_big192", 7: "bf16_big128"}
 
 
 def projection_variant(K: int, B: int, L: int, d: int, V: int, dtype: torch.dtype | int,

@@ -22,12 +22,18 @@ ProjPlan plan_projection(int dtype, long long rows_cap, int V) {
     // HBM-bound: one row tile holding every projected row, so W_U is read
     // once; a multiple of 256 equal vocabulary tiles, so every CU streams the
     // same share
-    p.variant = rows_cap <= 32 ? PROJ_BF16_S32 : rows_cap <= 64 ? PROJ_BF16_S64 : PROJ_BF16_S128;
-    p.rows_per_tile = rows_cap <= 32 ? 32 : rows_cap <= 64 ? 64 : 128;
+    p.variant = rows_cap <= 32 ? PROJ_BF16_S32 : PROJ_BF16_S64;
+    p.rows_per_tile = rows_cap <= 32 ? 32 : 64;
     p.vocab_cap = kStreamTileVocab;
     int nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
     nvt = ((nvt + 255) / 256) * 256;
     p.nvt = nvt < V ? nvt : V;
+  } else if (rows_cap <= kBigTileRowsMid) {
+    // one MFMA tile of 256 vocabulary rows x 128 projected rows per vocabulary tile
+    p.variant = PROJ_BF16_BIG128;
+    p.rows_per_tile = kBigTileRowsMid;
+    p.vocab_cap = kBigTileVocab;
+    p.nvt = (V + p.vocab_cap - 1) / p.vocab_cap;
   } else {
     // MFMA tiles of 256 vocabulary rows x 256 or 192 projected rows, whichever
     // pads the rows less (ties to 256)
@@ -49,10 +55,10 @@ hipError_t launch_projection(const Launch& a, hipStream_t s) {
   if (a.max_masked <= 0) return hipSuccess;
   switch (a.plan.variant) {
     case PROJ_BF16_S32:
-    case PROJ_BF16_S64:
-    case PROJ_BF16_S128: return launch_proj_stream(a, s);
+    case PROJ_BF16_S64: return launch_proj_stream(a, s);
     case PROJ_BF16_BIG:
-    case PROJ_BF16_BIG192: return launch_proj_big(a, s);
+    case PROJ_BF16_BIG192:
+    case PROJ_BF16_BIG128: return launch_proj_big(a, s);
     case PROJ_F32: return launch_proj_f32(a, s);
   }
   return hipErrorInvalidValue;

@@ -1,6 +1,6 @@
-// K1 projection, bf16, up to 256 projected rows: the regime where streaming
+// K1 projection, bf16, up to 64 projected rows: the regime where streaming
 // W_U once per call from HBM sets the time (the ridge of MI355X is about
-// 315 rows).
+// 315 rows; from 65 rows on the MFMA tile of proj_big.hip is faster).
 #include "rpd_device.h"
 
 namespace rpd {
@@ -88,9 +88,10 @@ __device__ int compact_in_workgroup(const CompactArgs& ca, int* s_pos, int need,
 // block and projected row 32*nb + (l & 31).
 //
 // Measured at the LLaDA-8B shape (d = 4096, V = 126464; projection alone,
-// best of several runs on one GPU): 156 us at 32 rows (83% of 8 TB/s),
-// 164 us at 64, 187-195 us at 104-128, 266-268 us at 160-192. Above 192 rows
-// the 256 x 256 MFMA tile is faster.
+// median of 60 calls on one GPU): 156 us at 32 rows (83% of 8 TB/s), 162-164
+// us at 48-64. An 8-wave form for 65..128 rows (256 vocabulary rows x 128
+// projected rows, one workgroup per CU) took 196-210 us at 68-128 rows, 7-12%
+// slower than the 256 x 128 MFMA tile, and is no longer built.
 //
 // FC: the workgroup compacts the mask itself (compact_in_workgroup).
 //
@@ -98,7 +99,7 @@ __device__ int compact_in_workgroup(const CompactArgs& ca, int* s_pos, int need,
 // W_U bytes in flight per CU (what the streaming rate depends on). The
 // 64-row form needs the launch bound's second argument for that (left to
 // itself the compiler took 185 VGPRs + 80 AGPRs, one workgroup per CU):
-// 4% faster at 64 rows. The 8-wave forms hold one workgroup per CU.
+// 4% faster at 64 rows.
 template <int NW, int MV, int NB, bool FC>
 __global__ __launch_bounds__(NW * 64, (NW == 4 && NB >= 2) ? 2 : 1) void k_proj_bf16_stream(
     const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w_u, const int32_t* __restrict__ rows,
@@ -327,7 +328,7 @@ void launch_stream(const Launch& a, hipStream_t s) {
 
 bool compact_fused(const Launch& a) {
   const ProjVariant v = a.plan.variant;
-  const bool streaming = v == PROJ_BF16_S32 || v == PROJ_BF16_S64 || v == PROJ_BF16_S128;
+  const bool streaming = v == PROJ_BF16_S32 || v == PROJ_BF16_S64;
   return streaming && a.plan.nrt == 1 && a.max_masked > 0 && (long long)a.B * a.L <= kFusedCompactMax &&
          !a.xrows && !a.rowoff;   // the normalization and explicit row lists need the compaction first
 }
@@ -336,7 +337,6 @@ hipError_t launch_proj_stream(const Launch& a, hipStream_t s) {
   switch (a.plan.variant) {
     case PROJ_BF16_S32: launch_stream<4, 2, 1>(a, s); break;
     case PROJ_BF16_S64: launch_stream<4, 2, 2>(a, s); break;
-    case PROJ_BF16_S128: launch_stream<8, 1, 4>(a, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

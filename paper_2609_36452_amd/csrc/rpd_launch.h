@@ -14,10 +14,10 @@ namespace rpd {
 enum ProjVariant {
   PROJ_BF16_S32 = 0,    // <= 32 rows: W_U streamed through wave-private LDS, hidden rows shared
   PROJ_BF16_S64 = 1,    // <= 64 rows, same kernel family
-  PROJ_BF16_S128 = 2,   // <= 128 rows
   PROJ_F32 = 3,         // fp32 inputs: vector ALU, 16 rows x 64 vocab
   PROJ_BF16_BIG = 4,    // MFMA-bound: 256 x 256 tiles, both operands staged through LDS
   PROJ_BF16_BIG192 = 6, // the same kernel with 256 x 192 tiles (where they pad the rows less)
+  PROJ_BF16_BIG128 = 7, // the same kernel with 256 x 128 tiles, for 65..128 rows
 };
 
 // tile of the large-row variant: vocabulary rows x projected rows
@@ -25,11 +25,13 @@ constexpr int kBigTileVocab = 256, kBigTileRows = 256;
 // vocabulary rows of one workgroup of the streaming variants (all of them)
 constexpr int kStreamTileVocab = 256;
 // most projected rows a streaming variant takes; above, the MFMA tiles are
-// faster (256 x 192 measured 3-8% faster than 192-row streaming at 132-192
-// rows, 256 x 256 7-9% faster than 256-row streaming at 224 and 256)
-constexpr int kStreamMaxRows = 128;
-// rows of the smaller MFMA tile
-constexpr int kBigTileRowsSmall = 192;
+// faster (256 x 128 measured 7-12% faster than 128-row streaming at 68-128
+// rows, 256 x 192 3-8% faster than 192-row streaming at 132-192 rows,
+// 256 x 256 7-9% faster than 256-row streaming at 224 and 256; at 48 and 64
+// rows the 64-row streaming form is 11% faster than 256 x 128)
+constexpr int kStreamMaxRows = 64;
+// rows of the smaller MFMA tiles
+constexpr int kBigTileRowsSmall = 192, kBigTileRowsMid = 128;
 // largest canvas (B * L) whose compaction the streaming projection does itself
 constexpr int kFusedCompactMax = 2048;
 
@@ -134,7 +136,7 @@ bool compact_fused(const Launch& a);
 // the projection variants, dispatched by launch_projection on a.plan.variant
 // the final normalization of the compacted rows into a.xrows (before the projection)
 hipError_t launch_norm_rows(const Launch& a, hipStream_t s);
-hipError_t launch_proj_stream(const Launch& a, hipStream_t s);  // PROJ_BF16_S32 .. PROJ_BF16_S128
+hipError_t launch_proj_stream(const Launch& a, hipStream_t s);  // PROJ_BF16_S32, PROJ_BF16_S64
 hipError_t launch_proj_big(const Launch& a, hipStream_t s);     // PROJ_BF16_BIG
 hipError_t launch_proj_f32(const Launch& a, hipStream_t s);     // PROJ_F32
 

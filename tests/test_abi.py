@@ -58,9 +58,9 @@ def test_workspace_size():
     # late-decode LLaDA shape: header + row list + (32 rows x 512 tiles of 256 vocabulary rows x 16 B)
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=8)
     assert n == 256 + 1024 + _a256(32 * 512 * 16) + _lazy(8)
-    # 10% masked: 104 rows x 512 tiles of 256 vocabulary rows
+    # 10% masked: 104 rows x 494 tiles of 256 vocabulary rows (one 128-row MFMA tile per vocabulary tile)
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=26)
-    assert n == 256 + 1024 + _a256(104 * 512 * 16) + _lazy(26)
+    assert n == 256 + 1024 + _a256(104 * 494 * 16) + _lazy(26)   # 65..128 rows: MFMA tiles, V / 256 of them
     # 100% masked: 1024 rows x 494 tiles of 256 vocabulary rows
     n = rpd.workspace_size(4, 1, 256, 4096, 126464, rpd.DTYPE_BF16, max_masked=256)
     assert n == 256 + 1024 + _a256(1024 * 494 * 16) + _lazy(256)
@@ -75,9 +75,9 @@ def test_workspace_size():
 def test_projection_variant_thresholds():
     pv = lambda n, dt=rpd.DTYPE_BF16: rpd.projection_variant(4, 1, 256, 4096, 126464, dt, max_masked=n)  # noqa: E731
     assert [pv(n) for n in (1, 8, 9, 16, 17, 32, 33, 48, 49, 64, 65, 256)] == \
-        ["bf16_s32", "bf16_s32", "bf16_s64", "bf16_s64", "bf16_s128", "bf16_s128", "bf16_big192", "bf16_big192",
+        ["bf16_s32", "bf16_s32", "bf16_s64", "bf16_s64", "bf16_big128", "bf16_big128", "bf16_big192", "bf16_big192",
          "bf16_big", "bf16_big", "bf16_big192", "bf16_big"]
-    # above 128 rows: the MFMA tile of 192 or 256 rows that pads the rows less (ties to 256)
+    # 65..128 rows: one 128-row MFMA tile; above: the tile of 192 or 256 rows that pads the rows less (ties to 256)
     assert [pv(n) for n in (96, 144, 192, 225)] == ["bf16_big192", "bf16_big192", "bf16_big", "bf16_big192"]
     assert pv(8, rpd.DTYPE_F32) == "f32" and pv(256, rpd.DTYPE_F32) == "f32"
     assert pv(-1) == "bf16_big"          # -1 plans for every position masked

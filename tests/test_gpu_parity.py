@@ -3,8 +3,8 @@
 Small and mid-size cases are compared element by element (every masked
 position, every layer); they span several vocabulary and row tiles, ragged
 vocabulary sizes and hidden sizes that are not multiples of the 64-wide
-k-chunk, and every projection variant (the streaming family at <= 32, 64
-and 128 projected rows, and the 192- and 256-row MFMA tiles above, with row
+k-chunk, and every projection variant (the streaming family at <= 32 and
+64 projected rows, and the 128-, 192- and 256-row MFMA tiles above, with row
 tiles split across XCDs, and rows gathered through 32-bit buffer offsets or,
 from a hidden tensor of more than 2^31 bytes, 64-bit addresses). Full-size LLaDA-8B / Dream-7B shapes are
 compared on sampled positions that the oracle computes one by one, plus the
@@ -65,7 +65,7 @@ BF16_CASES = [
     # rows = K * masked. Hidden sizes: whole 64-wide chunks, odd chunk counts, ragged tails.
     ("bf16_s32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
     ("bf16_s64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10, masked_frac=None), 12),
-    ("bf16_s128_long_d", dict(B=1, L=40, K=4, d=4104, V=2500, n_masked=20, masked_frac=None), 15),
+    ("bf16_big128_long_d", dict(B=1, L=40, K=4, d=4104, V=2500, n_masked=20, masked_frac=None), 15),
     ("bf16_big192_two_seqs", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=20, masked_frac=None), 16),
     ("bf16_big_one_row_tile_odd_chunks", dict(B=1, L=80, K=3, d=200, V=6007, n_masked=80, masked_frac=None), 17),
     ("bf16_big_vocab_split", dict(B=3, L=100, K=4, d=520, V=7001, n_masked=None, masked_frac=0.5), 13),
@@ -125,7 +125,7 @@ def _gain(w, seed):
     return round_bf16_bits(g) if w.cfg.dtype == "bf16" else g.astype(np.float32)
 
 
-NORM_CASES = [c for c in BF16_CASES if c[0] in ("bf16_s32", "bf16_s128_long_d", "bf16_big_one_row_tile_odd_chunks",
+NORM_CASES = [c for c in BF16_CASES if c[0] in ("bf16_s32", "bf16_big128_long_d", "bf16_big_one_row_tile_odd_chunks",
                                                "bf16_big_vocab_split")]
 
 
@@ -142,7 +142,7 @@ def test_final_normalization_prologue(name, ov, seed, norm_final):
 
 
 @pytest.mark.parametrize("scale", [0.5, 2.0])
-@pytest.mark.parametrize("name", ["bf16_s32", "bf16_s128_long_d", "bf16_big_vocab_split"])
+@pytest.mark.parametrize("name", ["bf16_s32", "bf16_big128_long_d", "bf16_big_vocab_split"])
 def test_logit_scale(name, scale):
     ov, seed = {c[0]: (c[1], c[2]) for c in BF16_CASES}[name]
     w = make_workload(CONFIGS["llada_late"].with_(name=name, **ov), seed)
@@ -159,7 +159,7 @@ def test_fp32_normalization_and_scale():
 # ------------------------------------------------------- lazy projection --
 
 LAZY_CASES = [("bf16_s32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, masked_frac=None), 11),
-              ("bf16_s128", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=16, masked_frac=None), 16),
+              ("bf16_big128", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=16, masked_frac=None), 16),
               ("bf16_big", dict(B=1, L=120, K=4, d=200, V=6007, n_masked=100, masked_frac=None), 17),
               # 200 positions: the final-layer pass lists 200 rows, which the 256 x 256 tile takes
               ("bf16_big_row_list", dict(B=1, L=240, K=4, d=136, V=3001, n_masked=200, masked_frac=None), 20)]
