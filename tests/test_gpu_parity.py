@@ -72,6 +72,9 @@ BF16_CASES = [
     ("bf16_big192_row_split", dict(B=4, L=600, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 14),
     ("bf16_big_row_split", dict(B=4, L=512, K=4, d=136, V=3001, n_masked=None, masked_frac=1.0), 22),
     ("bf16_big192_three_row_tiles", dict(B=2, L=100, K=4, d=264, V=3001, n_masked=72, masked_frac=None), 23),
+    ("bf16_big128_short_d", dict(B=1, L=60, K=3, d=56, V=3001, n_masked=40, masked_frac=None), 26),
+    ("bf16_big128_one_chunk", dict(B=1, L=60, K=4, d=64, V=2011, n_masked=30, masked_frac=None), 27),
+    ("bf16_big128_ragged_vocab_two_seqs", dict(B=2, L=50, K=4, d=328, V=6999, n_masked=12, masked_frac=None), 28),
     ("bf16_big192_short_d", dict(B=1, L=60, K=3, d=56, V=3001, n_masked=48, masked_frac=None), 24),
     ("bf16_big192_one_chunk", dict(B=1, L=60, K=3, d=64, V=2011, n_masked=48, masked_frac=None), 25),
     # the 256 x 256 tile with no full 64-wide chunk (only the zero-filled tail) and with exactly one
