@@ -16,26 +16,27 @@ namespace {
 //
 // Operands go from global memory straight into LDS (each load instruction
 // deposits 64 lanes x 16 B = 8 rows x 128 B of one operand at the LDS address
-// in M0), in 64-wide k-chunks, and are read back as MFMA fragments. W_U comes
-// through buffer loads (a resource at the tile's first row, fixed 32-bit lane
-// offsets, the chunk's offset in a scalar register: no per-load 64-bit address
-// arithmetic, 4% fewer loop cycles than global_load_lds with 64-bit lane
-// addresses); the gathered hidden rows through global_load_lds. No register staging and no LDS store instructions: with them,
-// the LDS instruction queue saturated (counters showed its data FIFO full
-// for 1.2e7 cycles per call at 1024 rows). The eight 16-byte pieces of row r
-// sit XOR-swizzled by (r >> 1) & 7 (each lane fetches the global piece that
-// belongs at its LDS slot), which keeps the fragment reads free of bank
-// conflicts.
+// in M0), in 64-wide k-chunks, and are read back as MFMA fragments. Both come
+// through buffer loads (a resource at W_U's tile or at the row source, fixed
+// 32-bit lane offsets, the chunk's offset in a scalar register: no per-load
+// 64-bit address arithmetic); a row source of 2^31 bytes or more takes
+// global_load_lds from 64-bit lane addresses instead (HB = false). No register
+// staging and no LDS store instructions: with them, the LDS instruction queue
+// saturated (counters showed its data FIFO full for 1.2e7 cycles per call at
+// 1024 rows). The eight 16-byte pieces of row r sit XOR-swizzled by
+// (r >> 1) & 7 (each lane fetches the global piece that belongs at its LDS
+// slot), which keeps the fragment reads free of bank conflicts.
 //
 // Stages: three for W_U (32 KB each) and two for the hidden rows (TR x 128 B
-// each): all 160 KB of LDS at TR = 256 (the epilogue's reduction array reuses
-// W_U stage 0). A
-// W_U chunk is first fetched from HBM by whichever of the workgroups sharing
-// it gets there first, while hidden rows mostly come from L2 or the MALL, so
-// W_U loads are issued two chunks earlier than hidden-row loads.
+// each): 160, 144 and 128 KB of LDS at TR = 256, 192 and 128 (the epilogue's
+// reduction array reuses W_U stage 0). A W_U chunk is first fetched from HBM
+// by whichever of the workgroups sharing it gets there first, while hidden
+// rows mostly come from L2 or the MALL, so W_U is loaded one chunk further
+// ahead than the hidden rows.
 //
 // Chunk c (W_U stage c % 3, hidden stage c % 2) is multiplied in four
-// k-steps of 16 MFMAs, each reading the next step's fragments. After the
+// k-steps of 4 * TR/64 MFMAs per wave, each reading the next step's
+// fragments. After the
 // third step every wave waits until only its newest 8 loads (W_U of chunk
 // c+2) may be outstanding, so chunk c+1 has landed, and for its fragment
 // reads; one barrier then publishes chunk c+1 and frees chunk c's stages
@@ -50,7 +51,8 @@ namespace {
 // the loads spread over the k-steps instead of all in the fourth: 12% fewer
 // cycles in the main loop, 3.5% less time (the chip then runs at its power
 // limit and lowers the clock); the epilogue without validity selects on full
-// tiles: 38% fewer epilogue cycles (10.2 ms at 12288 rows on one GPU).
+// tiles: 38% fewer epilogue cycles; buffer loads for W_U, then for the hidden
+// rows: 4% and 6% fewer main-loop cycles (9.5 ms at 12288 rows on one GPU).
 namespace big {
 constexpr int TV = kBigTileVocab, KC = 64;
 }  // namespace big
