@@ -72,7 +72,7 @@ typedef enum rpd_status {
  *               projects layers l0..L, Appendix A.6; here the K supplied)
  *   B, L        sequences and canvas positions per sequence (B >= 1, L >= 1,
  *               B*L <= 2^24)
- *   d, V        hidden size and vocabulary size (1 <= d, 1 <= V < 2^31);
+ *   d, V        hidden size and vocabulary size (1 <= d <= 2^20, 1 <= V < 2^31);
  *               bf16 requires d % 8 == 0
  *   dtype       RPD_DTYPE_BF16 or RPD_DTYPE_F32
  *   hidden      device [K][B][L][d]; hidden states already passed through the

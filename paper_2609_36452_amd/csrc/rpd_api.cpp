@@ -24,12 +24,15 @@ rpd_status fail(rpd_status s, const char* fmt, ...) {
 constexpr size_t kHeaderBytes = 256;   // n_masked (0), device status (4), lazy pass rows (12)
 constexpr long long kMaxBL = 1LL << 24;
 constexpr int kMaxK = 64;
+// hidden sizes up to 2^20: the MFMA tile's 32-bit byte offsets within its
+// 256 W_U rows (256 * d * 2) stay below 2^31
+constexpr int kMaxD = 1 << 20;
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 bool shape_ok(const rpd_problem* p) {
   return p->K >= 1 && p->K <= kMaxK && p->B >= 1 && p->L >= 1 && (long long)p->B * p->L <= kMaxBL && p->d >= 1 &&
-         p->V >= 1 && p->V < 0x7fffffff;
+         p->d <= kMaxD && p->V >= 1 && p->V < 0x7fffffff;
 }
 
 long long masked_cap(const rpd_problem* p) {
@@ -183,7 +186,7 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
   if (!p) return fail(RPD_ERR_NULL_POINTER, "problem is NULL");
   if (!p->hidden || !p->w_u || !p->mask) return fail(RPD_ERR_NULL_POINTER, "hidden, w_u and mask are required");
   if (!shape_ok(p))
-    return fail(RPD_ERR_BAD_SHAPE, "need 1<=K<=%d, B,L>=1, B*L<=2^24, d>=1, 1<=V<2^31-1 (got K=%d B=%d L=%d d=%d V=%d)",
+    return fail(RPD_ERR_BAD_SHAPE, "need 1<=K<=%d, B,L>=1, B*L<=2^24, 1<=d<=2^20, 1<=V<2^31-1 (got K=%d B=%d L=%d d=%d V=%d)",
                 kMaxK, p->K, p->B, p->L, p->d, p->V);
   if (p->dtype != RPD_DTYPE_BF16 && p->dtype != RPD_DTYPE_F32)
     return fail(RPD_ERR_UNSUPPORTED, "dtype %d is not supported", p->dtype);

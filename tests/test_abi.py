@@ -115,7 +115,8 @@ def _params(**kw):
 
 
 @pytest.mark.parametrize("kw,status", [
-    (dict(K=0), 2), (dict(K=65), 2), (dict(B=0), 2), (dict(L=0), 2), (dict(d=0), 2), (dict(V=0), 2),
+    (dict(K=0), 2), (dict(K=65), 2), (dict(B=0), 2), (dict(L=0), 2), (dict(d=0), 2), (dict(d=(1 << 20) + 8), 2),
+    (dict(V=0), 2),
     (dict(B=1 << 13, L=1 << 12), 2), (dict(dtype=3), 5), (dict(d=4100), 5), (dict(w_u=8200), 5),
     (dict(hidden=None), 1), (dict(mask=None), 1),
     (dict(norm_weight=8200), 5), (dict(norm_weight=8192, norm_eps=-1.0), 3),
