@@ -422,7 +422,8 @@ def _commit_property(g, mask, P):
 
 
 @pytest.mark.parametrize("cfgname,seed,nsample", [("llada_100", 2, 12), ("llada_25", 102, 12),
-                                                   ("llada_batched", 4, 10)])
+                                                   ("llada_10", 202, 12), ("llada_batched", 4, 10),
+                                                   ("llada_batched32", 204, 8)])
 def test_llada_full_size_sampled(cfgname, seed, nsample, llada_wu):
     w = make_workload(cfgname, seed, w_u=llada_wu)
     P = O.strict(4, 1.0)
