@@ -171,7 +171,8 @@ def bench_decode(args, w, P, hidden, w_u, mask, norm_kw) -> int:
     import torch
     from paper_2609_36452_amd import binding as rpd
     cfg = w.cfg
-    dec = rpd.Decoder(hidden, w_u, mask, P, graph=not P.lazy, sync_every=args.sync_every, **norm_kw)
+    # the decoder replays graphs unless a lazy call would read counts back (more than 256 masked)
+    dec = rpd.Decoder(hidden, w_u, mask, P, graph=True, sync_every=args.sync_every, **norm_kw)
     log(f"decode warmup {args.warmup} (first decode captures the plans)")
     r = None
     for _ in range(max(args.warmup, 1)):

@@ -143,9 +143,12 @@ typedef struct rpd_problem {
  * and so are persistence, drop and stability inside that band; outside it
  * they are not evaluated (persistence -1, drop and stability NaN), and the
  * per-layer outputs of layers never projected hold -1 / NaN. One projection
- * pass per layer (each streams W_U again) and one stream synchronisation
- * per pass after the first: it pays where the projection is compute-bound
- * (many masked positions), not where streaming W_U dominates.
+ * pass per layer (each streams W_U again): it pays where the projection is
+ * compute-bound (many masked positions), not where streaming W_U dominates.
+ * With max_masked <= 256 every pass is planned for that bound and reads its
+ * row count on the device, so the call never synchronises; with a larger
+ * bound it reads each pass's count back (one stream synchronisation per
+ * pass after the first) and plans the next pass for it.
  *
  * logit_scale multiplies every logit before the softmax statistics (an
  * inverse temperature). The paper reads probabilities before any
@@ -292,8 +295,9 @@ int32_t rpd_projection_variant(const rpd_problem* p);
  * commit or token, or step without progress, -> RPD_ERR_NULL_POINTER; B or L
  * < 1 or B*L > 2^24 -> RPD_ERR_BAD_SHAPE; progress_len < 0 ->
  * RPD_ERR_BAD_PARAM. Enqueued on `stream`; it allocates nothing and never
- * synchronises, so a loop body of rpd_score_commit (max_masked >= 0, lazy
- * projection off) followed by this call can be captured in a HIP graph.
+ * synchronises, so a loop body of rpd_score_commit (max_masked >= 0, and at
+ * most 256 with lazy projection) followed by this call can be captured in a
+ * HIP graph.
  */
 rpd_status rpd_apply_commit(int32_t B, int32_t L, uint8_t* mask, int32_t* canvas, const uint8_t* commit,
                             const int32_t* token, int32_t* progress, int32_t progress_len, int32_t* step,

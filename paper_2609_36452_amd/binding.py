@@ -353,8 +353,8 @@ class Decoder:
     every smaller bound of the same projection variant (down to half its
     bound for the variants whose grid grows with the rows). Plans are kept
     across ``reset()``, so repeated decodes replay the same graphs. Lazy
-    projection reads counts back inside the call, so it always runs
-    eagerly."""
+    projection with more than 256 masked positions reads counts back inside
+    the call, so that decode runs eagerly."""
 
     def __init__(self, hidden: torch.Tensor, w_u: torch.Tensor, mask: torch.Tensor, params: Params,
                  norm_weight: torch.Tensor | None = None, norm_eps: float = 1e-5, norm_final: bool = False,
@@ -363,13 +363,14 @@ class Decoder:
         _check_dev("mask", mask, (B, L), (torch.uint8, torch.bool))
         self.hidden, self.w_u, self.params = hidden, w_u, params
         self.norm = dict(norm_weight=norm_weight, norm_eps=norm_eps, norm_final=norm_final)
-        self.graph = bool(graph) and not params.lazy
         self.sync_every = max(1, int(sync_every))
         self.shape = (K, B, L, d, w_u.shape[0])
         dev = hidden.device
         self.mask0 = mask.view(torch.uint8).clone()
         self.mask = self.mask0.clone()
         self.n0 = int(self.mask0.sum().item())
+        # a lazy call reads nothing back while its bound (here at most n0) is at most 256
+        self.graph = bool(graph) and (not params.lazy or self.n0 <= 256)
         self.canvas = torch.full((B, L), -1, dtype=torch.int32, device=dev)
         self.step = torch.full((B, L), -1, dtype=torch.int32, device=dev)
         self.progress = torch.zeros(1 + max(self.n0, 1), dtype=torch.int32, device=dev)
