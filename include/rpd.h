@@ -145,10 +145,12 @@ typedef struct rpd_problem {
  * per-layer outputs of layers never projected hold -1 / NaN. One projection
  * pass per layer (each streams W_U again): it pays where the projection is
  * compute-bound (many masked positions), not where streaming W_U dominates.
- * With max_masked <= 256 every pass is planned for that bound and reads its
- * row count on the device, so the call never synchronises; with a larger
- * bound it reads each pass's count back (one stream synchronisation per
- * pass after the first) and plans the next pass for it.
+ * While the bound on a pass's rows (max_masked, then the last count read
+ * back) is at most 256, the pass reads its count on the device and is
+ * launched once per size class the count may fall in (<= 64, <= 128, up to
+ * the bound), all but one exiting at once; above, the previous pass's count
+ * is read back (one stream synchronisation) and the pass planned for it. So
+ * with max_masked <= 256 the call never synchronises.
  *
  * logit_scale multiplies every logit before the softmax statistics (an
  * inverse temperature). The paper reads probabilities before any

@@ -352,9 +352,9 @@ class Decoder:
     replayed: a plan is made for the first bound that needs it and serves
     every smaller bound of the same projection variant (down to half its
     bound for the variants whose grid grows with the rows). Plans are kept
-    across ``reset()``, so repeated decodes replay the same graphs. Lazy
-    projection with more than 256 masked positions reads counts back inside
-    the call, so that decode runs eagerly."""
+    across ``reset()``, so repeated decodes replay the same graphs. A lazy
+    call reads counts back while its bound exceeds 256 positions, so those
+    iterations run eagerly and the rest replay graphs."""
 
     def __init__(self, hidden: torch.Tensor, w_u: torch.Tensor, mask: torch.Tensor, params: Params,
                  norm_weight: torch.Tensor | None = None, norm_eps: float = 1e-5, norm_final: bool = False,
@@ -369,12 +369,11 @@ class Decoder:
         self.mask0 = mask.view(torch.uint8).clone()
         self.mask = self.mask0.clone()
         self.n0 = int(self.mask0.sum().item())
-        # a lazy call reads nothing back while its bound (here at most n0) is at most 256
-        self.graph = bool(graph) and (not params.lazy or self.n0 <= 256)
+        self.graph = bool(graph)
         self.canvas = torch.full((B, L), -1, dtype=torch.int32, device=dev)
         self.step = torch.full((B, L), -1, dtype=torch.int32, device=dev)
         self.progress = torch.zeros(1 + max(self.n0, 1), dtype=torch.int32, device=dev)
-        self._plans: dict[str, list] = {}   # variant -> [(bound, ScoreCommit, graph or None)]
+        self._plans: dict[tuple, list] = {}   # (variant, captured) -> [(bound, ScoreCommit, graph or None)]
         self.captures = 0
         self.bounds: list[int] = []    # the max_masked of each enqueued iteration
 
@@ -393,13 +392,15 @@ class Decoder:
     def _plan_for(self, bound: int):
         K, B, L, d, V = self.shape
         variant = projection_variant(K, B, L, d, V, self.hidden.dtype, max_masked=bound)
-        plans = self._plans.setdefault(variant, [])
+        # a lazy call reads counts back (and cannot be captured) while its bound exceeds 256
+        capture = self.graph and (not self.params.lazy or bound <= 256)
+        plans = self._plans.setdefault((variant, capture), [])
         fits = [p for p in plans if p[0] >= bound and (variant.startswith("bf16_s") or 2 * bound > p[0])]
         if fits:
             return min(fits, key=lambda p: p[0])
         sc = ScoreCommit(self.hidden, self.w_u, self.mask, self.params, max_masked=bound, **self.norm)
         g = None
-        if self.graph:
+        if capture:
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
                 self._iteration(sc)

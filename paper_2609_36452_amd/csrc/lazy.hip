@@ -80,12 +80,15 @@ __global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ p
 }
 
 // one workgroup: the positions still alive, in order, with the element
-// offsets of their layer-l rows; the count goes to *m_out. With first != 0
-// every position p < n is listed (the final-layer pass).
+// offsets of their layer-l rows; the count goes to *m_out and, as the count
+// of the one size class (<= t0, <= t1, above) it falls in, to tier[0..2]
+// (the others get 0). With first != 0 every position p < n is listed (the
+// final-layer pass).
 constexpr int kLazyNextThreads = 1024;
 __global__ __launch_bounds__(kLazyNextThreads) void k_lazy_next(const int32_t* __restrict__ n_ptr, LazyState st,
                                                                 const int32_t* __restrict__ rows, int l, int first,
-                                                                int B, int L, int d, int32_t* __restrict__ m_out) {
+                                                                int B, int L, int d, int32_t* __restrict__ m_out,
+                                                                int32_t* __restrict__ tier, int t0, int t1) {
   __shared__ int wsum[kLazyNextThreads / 64];
   const int n = *n_ptr;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
@@ -113,7 +116,12 @@ __global__ __launch_bounds__(kLazyNextThreads) void k_lazy_next(const int32_t* _
     carry += tot;
     __syncthreads();
   }
-  if (threadIdx.x == 0) *m_out = carry;
+  if (threadIdx.x == 0) {
+    *m_out = carry;
+    tier[0] = carry <= t0 ? carry : 0;
+    tier[1] = carry > t0 && carry <= t1 ? carry : 0;
+    tier[2] = carry > t1 ? carry : 0;
+  }
 }
 
 // Eq. 2-5 from the per-position state, one thread per masked position
@@ -156,13 +164,13 @@ __global__ __launch_bounds__(256) void k_lazy_score(const int32_t* __restrict__ 
 
 hipError_t launch_lazy_next(const Launch& a, int l, int first, hipStream_t s) {
   hipLaunchKernelGGL(k_lazy_next, dim3(1), dim3(kLazyNextThreads), 0, s, a.n_masked, a.lazy, a.rows, l, first, a.B,
-                     a.L, a.d, a.lazy.m);
+                     a.L, a.d, a.lazy.m, a.lazy.tier, kStreamMaxRows, kBigTileRowsMid);
   return hipGetLastError();
 }
 
 hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, hipStream_t s) {
   if (m_cap <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_lazy_reduce, dim3(m_cap), dim3(64), 0, s, a.partials, a.plan.nvt, a.lazy.m, a.lazy, l, a.K,
+  hipLaunchKernelGGL(k_lazy_reduce, dim3(m_cap), dim3(64), 0, s, a.partials, a.plan.nvt, a.n_masked, a.lazy, l, a.K,
                      a.B, a.L, a.rows, a.theta_c, a.theta_h, a.layer_argmax, a.layer_conf, a.layer_entropy);
   return hipGetLastError();
 }

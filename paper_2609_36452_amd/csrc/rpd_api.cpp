@@ -1,6 +1,7 @@
 // C ABI of the RPD commit step: argument validation, workspace layout,
 // launch planning and error reporting. Kernels live in proj_*.hip and
 // score_commit.hip; the projection plan in proj_plan.cpp.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -21,7 +22,7 @@ rpd_status fail(rpd_status s, const char* fmt, ...) {
   return s;
 }
 
-constexpr size_t kHeaderBytes = 256;   // n_masked (0), device status (4), lazy pass rows (12)
+constexpr size_t kHeaderBytes = 256;   // n_masked (0), device status (4), lazy pass rows (12), by size class (16)
 constexpr long long kMaxBL = 1LL << 24;
 constexpr int kMaxK = 64;
 // hidden sizes up to 2^20: the MFMA tile's 32-bit byte offsets within its
@@ -136,33 +137,47 @@ hipError_t run_lazy(rpd::Launch& a, int dtype, hipStream_t s, Mark& mark) {
   if (a.max_masked > 0) {
     if ((e = rpd::launch_lazy_next(a, a.K - 1, 1, s)) != hipSuccess) return e;
     int m_host = a.max_masked;   // pass 0 lists every projected position (<= max_masked)
-    // With at most 256 rows per pass every plan is one row tile across the
-    // whole vocabulary, however few rows a pass holds: each pass is then
-    // planned for the bound and takes its count from the device (a pass with
-    // none exits at once), and the call reads nothing back. Whole LLaDA-rule
-    // decodes measured 12% faster than with a read-back per pass. With more
-    // rows a pass planned for the bound would put its few row tiles on a few
-    // XCDs, so the count is read back and the next pass planned for it.
-    const bool bounded = a.max_masked <= rpd::kBigTileRows;
+    // A pass runs the plan for its row count, which only the device knows.
+    // While the bound on it is at most kLazyGateRows the host reads nothing
+    // back: the pass is launched once per size class the count may fall in
+    // (<= 64 rows: streaming; <= 128; up to the bound), each taking its
+    // count from the device as that class's count, 0 unless it is the
+    // class, so all but one exit at once. Above the bound the count is read
+    // back (one stream synchronisation) and the pass planned for it. A
+    // single pass planned for the bound would run an MFMA tile whatever the
+    // count (lazy call at 256 positions: 838 -> 1010 us), and above 256 rows
+    // its few row tiles would land on a few XCDs.
+    auto pass = [&](int l, int32_t* count, int cap) -> hipError_t {
+      rpd::Launch ap = a;
+      ap.n_masked = count;
+      ap.max_masked = cap;
+      ap.rowoff = a.lazy.rowoff;
+      ap.pass_layer = l;
+      ap.fused_compact = false;
+      ap.plan = rpd::plan_projection(dtype, cap, a.V);
+      hipError_t r;
+      if (ap.xrows && (r = rpd::launch_norm_rows(ap, s)) != hipSuccess) return r;
+      if ((r = rpd::launch_projection(ap, s)) != hipSuccess) return r;
+      return rpd::launch_lazy_reduce(ap, l, cap, s);
+    };
     for (int t = 0; t < a.K; ++t) {
       const int l = a.K - 1 - t;
-      if (t > 0 && !bounded) {
+      bool known = t == 0;
+      if (t > 0 && m_host > rpd::kLazyGateRows) {
         int32_t m = 0;
         if ((e = hipMemcpyAsync(&m, a.lazy.m, sizeof m, hipMemcpyDeviceToHost, s)) != hipSuccess) return e;
         if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
         if (m <= 0) break;
         m_host = m;
+        known = true;
       }
-      rpd::Launch ap = a;
-      ap.n_masked = a.lazy.m;
-      ap.max_masked = m_host;
-      ap.rowoff = a.lazy.rowoff;
-      ap.pass_layer = l;
-      ap.fused_compact = false;
-      ap.plan = rpd::plan_projection(dtype, m_host, a.V);
-      if (ap.xrows && (e = rpd::launch_norm_rows(ap, s)) != hipSuccess) return e;
-      if ((e = rpd::launch_projection(ap, s)) != hipSuccess) return e;
-      if ((e = rpd::launch_lazy_reduce(ap, l, m_host, s)) != hipSuccess) return e;
+      if (known || m_host <= rpd::kStreamMaxRows) {
+        if ((e = pass(l, a.lazy.m, m_host)) != hipSuccess) return e;
+      } else {
+        if ((e = pass(l, a.lazy.tier, rpd::kStreamMaxRows)) != hipSuccess) return e;
+        if ((e = pass(l, a.lazy.tier + 1, std::min(m_host, rpd::kBigTileRowsMid))) != hipSuccess) return e;
+        if (m_host > rpd::kBigTileRowsMid && (e = pass(l, a.lazy.tier + 2, m_host)) != hipSuccess) return e;
+      }
       if (l > 0 && (e = rpd::launch_lazy_next(a, l - 1, 0, s)) != hipSuccess) return e;
     }
   }
@@ -265,6 +280,7 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
       lz += a4;
     }
     a.lazy.m = reinterpret_cast<int32_t*>(ws + 12);
+    a.lazy.tier = reinterpret_cast<int32_t*>(ws + 16);
   }
   a.rowoff = nullptr;
   const bool lazy = (q->flags & RPD_PARAM_LAZY) != 0;

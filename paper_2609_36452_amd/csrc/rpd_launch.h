@@ -32,6 +32,8 @@ constexpr int kStreamTileVocab = 256;
 constexpr int kStreamMaxRows = 64;
 // rows of the smaller MFMA tiles
 constexpr int kBigTileRowsSmall = 192, kBigTileRowsMid = 128;
+// largest bound on a lazy pass's rows below which the host reads no count back
+constexpr int kLazyGateRows = 256;
 // largest canvas (B * L) whose compaction the streaming projection does itself
 constexpr int kFusedCompactMax = 2048;
 
@@ -61,6 +63,7 @@ struct LazyState {
   int32_t* alive;      // [cap] 1 while the walk continues
   int32_t* depth;      // [cap] layers projected
   int32_t* m;          // [1] rows in the current pass
+  int32_t* tier;       // [3] the same count in its size class (<= 64, <= 128, above), 0 in the others
 };
 
 struct LazyScoreArgs {

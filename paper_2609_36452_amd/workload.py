@@ -61,7 +61,7 @@ class WorkloadConfig:
     dtype: str                      # "bf16" or "f32"
     masked_frac: float | None = None  # fraction of L masked per sequence
     n_masked: int | None = None       # or an exact count per sequence
-    sharp: tuple = ("uniform", 0.0, 8.0)  # ("uniform", lo, hi) | ("ushape", smax) | ("calibrated",)
+    sharp: tuple = ("uniform", 0.0, 8.0)  # ("uniform", lo, hi) | ("ushape", smax) | ("calibrated"[, lo, hi])
     unstable_frac: float = 0.4
     layer_jitter: float = 0.5       # calibrated mode only: std of per-layer level jitter
 
@@ -202,9 +202,11 @@ def _sharpness(cfg: WorkloadConfig, g: np.random.Generator, pos: np.ndarray) -> 
         u = 2.0 * pos / max(cfg.L - 1, 1) - 1.0
         return cfg.sharp[1] * u * u * g.uniform(0.5, 1.0, size=pos.size)
     if kind == "calibrated":
-        # target-logit level spanning low to saturated confidence
+        # target-logit level spanning low to saturated confidence (by default
+        # ln V - 3 to ln V + 6; ("calibrated", lo, hi) sets the offsets)
         lnv = math.log(cfg.V)
-        return g.uniform(lnv - 3.0, lnv + 6.0, size=pos.size)
+        lo, hi = (cfg.sharp[1], cfg.sharp[2]) if len(cfg.sharp) == 3 else (-3.0, 6.0)
+        return g.uniform(lnv + lo, lnv + hi, size=pos.size)
     raise ValueError(kind)
 
 

@@ -165,14 +165,21 @@ LAZY_CASES = [("bf16_s32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8, maske
               ("bf16_big128", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=16, masked_frac=None), 16),
               ("bf16_big", dict(B=1, L=120, K=4, d=200, V=6007, n_masked=100, masked_frac=None), 17),
               # 200 positions: the final-layer pass lists 200 rows, which the 256 x 256 tile takes
-              ("bf16_big_row_list", dict(B=1, L=240, K=4, d=136, V=3001, n_masked=200, masked_frac=None), 20)]
+              ("bf16_big_row_list", dict(B=1, L=240, K=4, d=136, V=3001, n_masked=200, masked_frac=None), 20),
+              # most positions in the band: the passes after the first list 65-256 rows, launched once per
+              # size class (<= 64, <= 128, above) with the count taken on the device
+              ("bf16_size_classes", dict(B=1, L=256, K=5, d=136, V=3001, n_masked=250, masked_frac=None,
+                                         sharp=("calibrated", 0.5, 2.5), unstable_frac=0.1), 21),
+              # above 256 positions the second pass reads its count back, later ones run per size class
+              ("bf16_readback", dict(B=2, L=160, K=5, d=136, V=3001, n_masked=150, masked_frac=None,
+                                     sharp=("calibrated", 0.5, 2.5), unstable_frac=0.1), 22)]
 
 
 @pytest.mark.parametrize("name,ov,seed", LAZY_CASES, ids=[c[0] for c in LAZY_CASES])
 def test_lazy_projection(name, ov, seed):
     # Appendix A.6 "Layerwise projection": intermediate layers only inside the band theta_c <= c < theta_h,
     # down to the first disagreement; decisions are the eager ones
-    base = CONFIGS["llada_late"].with_(name="lazy_" + name, **ov).with_(sharp=("calibrated",), unstable_frac=0.4)
+    base = CONFIGS["llada_late"].with_(name="lazy_" + name, sharp=("calibrated",), unstable_frac=0.4).with_(**ov)
     w = make_workload(base, seed)
     for P in (dataclasses.replace(O.LLADA, lazy=True), dataclasses.replace(O.DREAM, lazy=True, block=32)):
         g, o, _ = _check(w, P)
@@ -189,6 +196,12 @@ def test_lazy_projection_with_normalization_and_fp32():
     wb = make_workload(CONFIGS["llada_late"].with_(name="lazy_norm", B=1, L=64, K=4, d=264, V=5003, n_masked=8,
                                                    masked_frac=None, sharp=("calibrated",), unstable_frac=0.4), 12)
     _check(wb, dataclasses.replace(O.LLADA, lazy=True), norm=(_gain(wb, 4), 1e-5, True))
+    # 200 positions, most in the band: the passes after the first run once per size class, each
+    # normalizing only its rows
+    wc = make_workload(CONFIGS["llada_late"].with_(name="lazy_norm_classes", B=1, L=208, K=4, d=200, V=6007,
+                                                   n_masked=200, masked_frac=None, sharp=("calibrated", 0.5, 2.5),
+                                                   unstable_frac=0.1), 13)
+    _check(wc, dataclasses.replace(O.LLADA, lazy=True), norm=(_gain(wc, 5), 1e-5, False))
 
 
 # ------------------------------------------------------------- edge cases --
