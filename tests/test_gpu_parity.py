@@ -234,6 +234,17 @@ def test_budget_extremes(beta):
     _check(w, P)
 
 
+@pytest.mark.parametrize("n_masked", [4, 3])
+def test_small_call_four_sequences(n_masked):
+    # a late-decode call over four sequences (64 and 48 projected rows, the 64-row streaming form): budget,
+    # RPD-block and fallback per sequence
+    w = _small_bf16(seed=9, B=4, L=64, n_masked=n_masked)
+    for P in (O.LLADA, O.Params(theta_s=3.5, w=15.0, block=32), O.strict(4, 0.5),
+              O.Params(beta=0.0, theta_h=0.999999, theta_c=0.999998)):
+        g, o, _ = _check(w, P)
+        assert (g["n_commit"] >= 1).all()
+
+
 def test_fewer_masked_than_window_and_tiny_window():
     w = _small_bf16(seed=8, n_masked=5)
     _check(w, O.Params(beta=0.0, theta_h=0.999999, theta_c=0.999998))
