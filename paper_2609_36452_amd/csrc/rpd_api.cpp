@@ -127,9 +127,9 @@ void fill_common(rpd::Launch& a, const rpd_params* q, const rpd_outputs* o) {
 }
 
 // Lazy layerwise projection: one projection pass per layer from the final
-// one down over the positions still walking their agreement suffix; the
-// count of each later pass is read back (one stream synchronisation per
-// pass) to plan it, and the walk ends when it reaches zero.
+// one down over the positions still walking their agreement suffix (rows
+// listed by k_lazy_next); how a pass is planned for a count that only the
+// device knows is described in the loop.
 template <class Mark>
 hipError_t run_lazy(rpd::Launch& a, int dtype, hipStream_t s, Mark& mark) {
   hipError_t e = mark(1);
