@@ -296,6 +296,7 @@ __device__ __forceinline__ void commit_sequence(const uint8_t* __restrict__ mask
     const bool masked = in && mask[o] != 0;
     const unsigned fl_in = in ? sc.flag(o) : 0u;
     const float H_in = in ? sc.ent(o) : 0.f;
+    const float c_in = in ? sc.conf(o) : 0.f;
     const unsigned fl = masked ? fl_in : 0u;
     const bool cand = (fl & kFlagCandidate) != 0;
     const float H = masked ? H_in : 0.f;
@@ -317,8 +318,7 @@ __device__ __forceinline__ void commit_sequence(const uint8_t* __restrict__ mask
         a.flags[o] = (uint8_t)(fl | (com ? kFlagCommitted : 0u));
         a.upstream_entropy[o] = E_i;
         if (a.block > 0 ? in_block : (rank < a.window)) {
-          float cv = sc.conf(o);
-          cv = (cv != cv) ? -INFINITY : cv;
+          const float cv = (c_in != c_in) ? -INFINITY : c_in;
           if (cv > best_c || (cv == best_c && i < best_i)) {
             best_c = cv;
             best_i = i;
@@ -397,8 +397,11 @@ __global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4
   __shared__ float lc[64], lh[64];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int p = blockIdx.x;
+  // The count, the row and the partials are loaded together: workgroup p <
+  // max_masked reads inside the rows and partials buffers (sized for
+  // max_masked positions) whatever the count, and a workgroup beyond the
+  // count drops what it read.
   const int n = *n_ptr;
-  if (p >= n) return;
   {
     const int pos = rows[p];
     const int b = pos / a.L, i = pos - b * a.L;
@@ -406,6 +409,7 @@ __global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4
       const Soft s = wave_merge_row(partials + ((long long)p * a.K + l) * nvt, nvt, lane);
       if (lane == 0) state_stats(s, ly[l], lc[l], lh[l]);
     }
+    if (p >= n) return;
     __syncthreads();
     if (wid == 0) {
       const int my_y = lane < a.K ? ly[lane] : -1;
