@@ -12,8 +12,8 @@
 // table of element offsets into the hidden states, or normalized rows),
 // followed by k_lazy_reduce (merge the tile states, update each position's
 // suffix length and peak probability) and k_lazy_next (list the positions
-// still alive with the row offsets of the next layer; the host reads their
-// count back to plan the next pass and stops at zero). k_lazy_score then
+// still alive with the row offsets of the next layer, and their count; the
+// host plans the next pass for a bound on it or reads it back). k_lazy_score then
 // evaluates Eq. 2-5 from the per-position state, with persistence exact for
 // every position of the band; outside it stability is not evaluated
 // (persistence -1, drop and stability NaN). The commitment follows as usual.
@@ -47,13 +47,22 @@ __global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ p
                                                     float theta_h, int32_t* __restrict__ layer_argmax,
                                                     float* __restrict__ layer_conf, float* __restrict__ layer_entropy) {
   const int j = blockIdx.x, lane = threadIdx.x;
-  if (j >= *m_ptr) return;
+  // the row's position is loaded with the count (j < m_cap stays inside act),
+  // and the position's state with the tile states (unused in the final-layer
+  // pass): two memory round trips before the update instead of four. A
+  // workgroup beyond the count (most of them in the passes of the size
+  // classes the count is not in) exits before reading anything else.
+  const int m = *m_ptr;
+  const int p = st.act[j];
+  if (j >= m) return;
+  const int y_prev = st.y[p], k_prev = st.k[p];
+  const float pmax_prev = st.pmax[p];
+  const int pos = layer_argmax ? rows[p] : 0;
   const Soft s = lazy_merge_row(partials + (long long)j * nvt, nvt, lane);
   if (lane != 0) return;
   const int y = (s.idx == INT_MAX) ? -1 : s.idx;
   const float c = 1.0f / s.S;
   const float h = (s.S != s.S) ? s.S : fmaxf(logf(s.S) - s.T / s.S, 0.0f);
-  const int p = st.act[j];
   if (l == K - 1) {
     st.y[p] = y;
     st.c[p] = c;
@@ -61,16 +70,15 @@ __global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ p
     st.k[p] = 1;
     st.pmax[p] = c;
     st.alive[p] = (K > 1 && c >= theta_c && c < theta_h) ? 1 : 0;   // NaN fails
-  } else if (y == st.y[p]) {
-    st.k[p] += 1;
-    st.pmax[p] = fmaxf(st.pmax[p], c);
+  } else if (y == y_prev) {
+    st.k[p] = k_prev + 1;
+    st.pmax[p] = fmaxf(pmax_prev, c);
     st.alive[p] = l > 0 ? 1 : 0;
   } else {
     st.alive[p] = 0;
   }
   st.depth[p] = K - l;
   if (layer_argmax) {
-    const int pos = rows[p];
     const int b = pos / L, i = pos - b * L;
     const long long ol = ((long long)l * B + b) * L + i;
     layer_argmax[ol] = y;
@@ -86,16 +94,23 @@ __global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ p
 // final-layer pass).
 constexpr int kLazyNextThreads = 1024;
 __global__ __launch_bounds__(kLazyNextThreads) void k_lazy_next(const int32_t* __restrict__ n_ptr, LazyState st,
-                                                                const int32_t* __restrict__ rows, int l, int first,
-                                                                int B, int L, int d, int32_t* __restrict__ m_out,
-                                                                int32_t* __restrict__ tier, int t0, int t1) {
+                                                                const int32_t* __restrict__ rows, int cap, int l,
+                                                                int first, int B, int L, int d,
+                                                                int32_t* __restrict__ m_out, int32_t* __restrict__ tier,
+                                                                int t0, int t1) {
   __shared__ int wsum[kLazyNextThreads / 64];
-  const int n = *n_ptr;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  // the first chunk's state and row are loaded with the count (p < cap stays
+  // inside both buffers; entries at or beyond the count are not used)
+  const bool in0 = (int)threadIdx.x < cap;
+  const int alive0 = (in0 && !first) ? st.alive[threadIdx.x] : 1;
+  const int row0 = in0 ? rows[threadIdx.x] : 0;
+  const int n = *n_ptr;
   int carry = 0;
   for (int base = 0; base < n; base += blockDim.x) {
     const int p = base + threadIdx.x;
-    const bool f = p < n && (first || st.alive[p] != 0);
+    const int alive = base == 0 ? alive0 : (p < n && !first ? st.alive[p] : 1);
+    const bool f = p < n && (first || alive != 0);
     const unsigned long long bal = __ballot(f);
     const int before = __popcll(bal & ((1ull << lane) - 1ull));
     if (lane == 0) wsum[wid] = __popcll(bal);
@@ -108,7 +123,7 @@ __global__ __launch_bounds__(kLazyNextThreads) void k_lazy_next(const int32_t* _
     }
     if (f) {
       const int j = carry + off + before;
-      const int pos = rows[p];
+      const int pos = base == 0 ? row0 : rows[p];
       const int b = pos / L, i = pos - b * L;
       st.act[j] = p;
       st.rowoff[j] = (((long long)l * B + b) * L + i) * (long long)d;
@@ -163,8 +178,8 @@ __global__ __launch_bounds__(256) void k_lazy_score(const int32_t* __restrict__ 
 }  // namespace
 
 hipError_t launch_lazy_next(const Launch& a, int l, int first, hipStream_t s) {
-  hipLaunchKernelGGL(k_lazy_next, dim3(1), dim3(kLazyNextThreads), 0, s, a.n_masked, a.lazy, a.rows, l, first, a.B,
-                     a.L, a.d, a.lazy.m, a.lazy.tier, kStreamMaxRows, kBigTileRowsMid);
+  hipLaunchKernelGGL(k_lazy_next, dim3(1), dim3(kLazyNextThreads), 0, s, a.n_masked, a.lazy, a.rows, a.max_masked, l,
+                     first, a.B, a.L, a.d, a.lazy.m, a.lazy.tier, kStreamMaxRows, kBigTileRowsMid);
   return hipGetLastError();
 }
 
