@@ -40,3 +40,15 @@ def test_bf16_config_small():
     h = bf16_bits_to_f32(w.hidden[:, 0, w.mask[0] == 1])
     assert np.isfinite(h).all()
     assert w.mask.sum() == 8
+
+
+def test_calibrated_level_range():
+    # calibrated mode draws the target-logit level from ln V + U(lo, hi): (-3, 6) by default, or the
+    # offsets given in the sharpness tuple (the lazy-projection cases narrow it to fill the band)
+    base = CONFIGS["llada_late"].with_(d=64, V=1000, L=200, n_masked=150, masked_frac=None)
+    lnv = np.log(1000.0)
+    for sharp, lo, hi in ((("calibrated",), -3.0, 6.0), (("calibrated", 0.5, 2.5), 0.5, 2.5)):
+        w = make_workload(base.with_(sharp=sharp), 4)
+        s = np.concatenate(w.meta["sharpness"])
+        assert s.size == 150 and (s >= lnv + lo).all() and (s < lnv + hi).all()
+        assert s.max() - s.min() > 0.8 * (hi - lo)     # spread over the range, not a point
