@@ -232,6 +232,10 @@ def bench_decode(args, w, P, hidden, w_u, mask, norm_kw) -> int:
                 "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4)}
     roof["traffic"] = None
     roof["kernel"] = f"projection launches of the {dom}-bound iterations (varying variant)"
+    # the lazy passes project only the rows still walking their suffix, a count the host never sees:
+    # their rate is then stated against the eager work of the same iterations, not their own
+    roof["work_basis"] = ("eager-equivalent: 2*K*n*V*d flops and V*d + K*n*d elements per iteration; the lazy "
+                          "passes do less, so this overstates their own rate") if P.lazy else "algorithmic"
     roof["iterations"] = sum(1 for n in counts if (n * cfg.K < RIDGE_ROWS) == (dom == "hbm"))
     roof["kernel_ms_per_decode"] = round(ms_sum, 4)
     roof["projection_ms_per_decode"] = round(float(np.sum(proj)), 4)
