@@ -41,7 +41,8 @@ __device__ __forceinline__ Soft lazy_merge_row(const float4* __restrict__ src, i
 
 // one wave per row j < m of the pass (layer l): statistics of the row, then
 // the update of its position's state
-__global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ partials, int nvt,
+__global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ partials, int nvt0, int nvt1,
+                                                    int nvt2, int t0, int t1,
                                                     const int32_t* __restrict__ m_ptr, LazyState st, int l, int K,
                                                     int B, int L, const int32_t* __restrict__ rows, float theta_c,
                                                     float theta_h, int32_t* __restrict__ layer_argmax,
@@ -55,6 +56,9 @@ __global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ p
   const int m = *m_ptr;
   const int p = st.act[j];
   if (j >= m) return;
+  // the partials follow the plan of the size class the count is in (<= t0,
+  // <= t1, above; one plan when the pass was launched once)
+  const int nvt = m <= t0 ? nvt0 : (m <= t1 ? nvt1 : nvt2);
   const int y_prev = st.y[p], k_prev = st.k[p];
   const float pmax_prev = st.pmax[p];
   const int pos = layer_argmax ? rows[p] : 0;
@@ -183,9 +187,12 @@ hipError_t launch_lazy_next(const Launch& a, int l, int first, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, hipStream_t s) {
+hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, const int* nvt_class, hipStream_t s) {
   if (m_cap <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_lazy_reduce, dim3(m_cap), dim3(64), 0, s, a.partials, a.plan.nvt, a.n_masked, a.lazy, l, a.K,
+  const int n0 = nvt_class ? nvt_class[0] : a.plan.nvt, n1 = nvt_class ? nvt_class[1] : a.plan.nvt,
+            n2 = nvt_class ? nvt_class[2] : a.plan.nvt;
+  hipLaunchKernelGGL(k_lazy_reduce, dim3(m_cap), dim3(64), 0, s, a.partials, n0, n1, n2, kStreamMaxRows,
+                     kBigTileRowsMid, a.n_masked, a.lazy, l, a.K,
                      a.B, a.L, a.rows, a.theta_c, a.theta_h, a.layer_argmax, a.layer_conf, a.layer_entropy);
   return hipGetLastError();
 }

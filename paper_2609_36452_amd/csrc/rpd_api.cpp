@@ -147,7 +147,8 @@ hipError_t run_lazy(rpd::Launch& a, int dtype, hipStream_t s, Mark& mark) {
     // single pass planned for the bound would run an MFMA tile whatever the
     // count (lazy call at 256 positions: 838 -> 1010 us), and above 256 rows
     // its few row tiles would land on a few XCDs.
-    auto pass = [&](int l, int32_t* count, int cap) -> hipError_t {
+    // a pass over `cap` rows whose count is at `count`
+    auto pass_launch = [&](int l, int32_t* count, int cap) {
       rpd::Launch ap = a;
       ap.n_masked = count;
       ap.max_masked = cap;
@@ -155,10 +156,7 @@ hipError_t run_lazy(rpd::Launch& a, int dtype, hipStream_t s, Mark& mark) {
       ap.pass_layer = l;
       ap.fused_compact = false;
       ap.plan = rpd::plan_projection(dtype, cap, a.V);
-      hipError_t r;
-      if (ap.xrows && (r = rpd::launch_norm_rows(ap, s)) != hipSuccess) return r;
-      if ((r = rpd::launch_projection(ap, s)) != hipSuccess) return r;
-      return rpd::launch_lazy_reduce(ap, l, cap, s);
+      return ap;
     };
     for (int t = 0; t < a.K; ++t) {
       const int l = a.K - 1 - t;
@@ -171,12 +169,24 @@ hipError_t run_lazy(rpd::Launch& a, int dtype, hipStream_t s, Mark& mark) {
         m_host = m;
         known = true;
       }
+      // the pass's rows are normalized once and reduced once; in between one
+      // projection, or one per size class, of which only the count's class
+      // writes the partials (the reduction takes that class's layout)
+      const rpd::Launch whole = pass_launch(l, a.lazy.m, m_host);
+      if (whole.xrows && (e = rpd::launch_norm_rows(whole, s)) != hipSuccess) return e;
       if (known || m_host <= rpd::kStreamMaxRows) {
-        if ((e = pass(l, a.lazy.m, m_host)) != hipSuccess) return e;
+        if ((e = rpd::launch_projection(whole, s)) != hipSuccess) return e;
+        if ((e = rpd::launch_lazy_reduce(whole, l, m_host, nullptr, s)) != hipSuccess) return e;
       } else {
-        if ((e = pass(l, a.lazy.tier, rpd::kStreamMaxRows)) != hipSuccess) return e;
-        if ((e = pass(l, a.lazy.tier + 1, std::min(m_host, rpd::kBigTileRowsMid))) != hipSuccess) return e;
-        if (m_host > rpd::kBigTileRowsMid && (e = pass(l, a.lazy.tier + 2, m_host)) != hipSuccess) return e;
+        const int caps[3] = {rpd::kStreamMaxRows, std::min(m_host, rpd::kBigTileRowsMid), m_host};
+        const int ncls = m_host > rpd::kBigTileRowsMid ? 3 : 2;
+        int nvt[3];
+        for (int c = 0; c < 3; ++c) {
+          const rpd::Launch ap = pass_launch(l, a.lazy.tier + c, caps[c]);
+          nvt[c] = ap.plan.nvt;
+          if (c < ncls && (e = rpd::launch_projection(ap, s)) != hipSuccess) return e;
+        }
+        if ((e = rpd::launch_lazy_reduce(whole, l, m_host, nvt, s)) != hipSuccess) return e;
       }
       if (l > 0 && (e = rpd::launch_lazy_next(a, l - 1, 0, s)) != hipSuccess) return e;
     }

@@ -130,7 +130,9 @@ hipError_t launch_commit(const Launch& a, hipStream_t s);
 // lazy layerwise projection: list the rows of layer l (first: every position),
 // reduce a pass over layer l, score from the per-position state
 hipError_t launch_lazy_next(const Launch& a, int l, int first, hipStream_t s);
-hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, hipStream_t s);
+// nvt_class: the vocabulary-tile counts of the plans for rows <= 64, <= 128
+// and above, when the pass ran once per size class (NULL: a.plan's)
+hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, const int* nvt_class, hipStream_t s);
 hipError_t launch_lazy_score(const Launch& a, hipStream_t s);
 // the projection does the compaction itself (needs a.plan and a.max_masked
 // >= 0): the call then launches no compaction kernel
