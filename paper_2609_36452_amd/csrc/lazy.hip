@@ -94,12 +94,12 @@ __global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ p
 // one workgroup: the positions still alive, in order, with the element
 // offsets of their layer-l rows; the count goes to *m_out and, as the count
 // of the one size class (<= t0, <= t1, above) it falls in, to tier[0..2]
-// (the others get 0). With first != 0 every position p < n is listed (the
-// final-layer pass).
+// (the others get 0). The final-layer pass, every masked position, is
+// listed by the compaction.
 constexpr int kLazyNextThreads = 1024;
 __global__ __launch_bounds__(kLazyNextThreads) void k_lazy_next(const int32_t* __restrict__ n_ptr, LazyState st,
                                                                 const int32_t* __restrict__ rows, int cap, int l,
-                                                                int first, int B, int L, int d,
+                                                                int B, int L, int d,
                                                                 int32_t* __restrict__ m_out, int32_t* __restrict__ tier,
                                                                 int t0, int t1) {
   __shared__ int wsum[kLazyNextThreads / 64];
@@ -107,14 +107,14 @@ __global__ __launch_bounds__(kLazyNextThreads) void k_lazy_next(const int32_t* _
   // the first chunk's state and row are loaded with the count (p < cap stays
   // inside both buffers; entries at or beyond the count are not used)
   const bool in0 = (int)threadIdx.x < cap;
-  const int alive0 = (in0 && !first) ? st.alive[threadIdx.x] : 1;
+  const int alive0 = in0 ? st.alive[threadIdx.x] : 0;
   const int row0 = in0 ? rows[threadIdx.x] : 0;
   const int n = *n_ptr;
   int carry = 0;
   for (int base = 0; base < n; base += blockDim.x) {
     const int p = base + threadIdx.x;
-    const int alive = base == 0 ? alive0 : (p < n && !first ? st.alive[p] : 1);
-    const bool f = p < n && (first || alive != 0);
+    const int alive = base == 0 ? alive0 : (p < n ? st.alive[p] : 0);
+    const bool f = p < n && alive != 0;
     const unsigned long long bal = __ballot(f);
     const int before = __popcll(bal & ((1ull << lane) - 1ull));
     if (lane == 0) wsum[wid] = __popcll(bal);
@@ -181,9 +181,9 @@ __global__ __launch_bounds__(256) void k_lazy_score(const int32_t* __restrict__ 
 
 }  // namespace
 
-hipError_t launch_lazy_next(const Launch& a, int l, int first, hipStream_t s) {
+hipError_t launch_lazy_next(const Launch& a, int l, hipStream_t s) {
   hipLaunchKernelGGL(k_lazy_next, dim3(1), dim3(kLazyNextThreads), 0, s, a.n_masked, a.lazy, a.rows, a.max_masked, l,
-                     first, a.B, a.L, a.d, a.lazy.m, a.lazy.tier, kStreamMaxRows, kBigTileRowsMid);
+                     a.B, a.L, a.d, a.lazy.m, a.lazy.tier, kStreamMaxRows, kBigTileRowsMid);
   return hipGetLastError();
 }
 

@@ -135,8 +135,7 @@ hipError_t run_lazy(rpd::Launch& a, int dtype, hipStream_t s, Mark& mark) {
   hipError_t e = mark(1);
   if (e != hipSuccess) return e;
   if (a.max_masked > 0) {
-    if ((e = rpd::launch_lazy_next(a, a.K - 1, 1, s)) != hipSuccess) return e;
-    int m_host = a.max_masked;   // pass 0 lists every projected position (<= max_masked)
+    int m_host = a.max_masked;   // pass 0, listed by the compaction: every masked position (<= max_masked)
     // A pass runs the plan for its row count, which only the device knows.
     // While the bound on it is at most kLazyGateRows the host reads nothing
     // back: the pass is launched once per size class the count may fall in
@@ -188,7 +187,7 @@ hipError_t run_lazy(rpd::Launch& a, int dtype, hipStream_t s, Mark& mark) {
         }
         if ((e = rpd::launch_lazy_reduce(whole, l, m_host, nvt, s)) != hipSuccess) return e;
       }
-      if (l > 0 && (e = rpd::launch_lazy_next(a, l - 1, 0, s)) != hipSuccess) return e;
+      if (l > 0 && (e = rpd::launch_lazy_next(a, l - 1, s)) != hipSuccess) return e;
     }
   }
   if ((e = mark(2)) != hipSuccess) return e;
@@ -308,7 +307,7 @@ static rpd_status score_commit_impl(const rpd_problem* p, const rpd_params* q, c
     a.fused_compact = !lazy && rpd::compact_fused(a);
   }
   hipError_t e = mark(0);
-  if (e == hipSuccess && !a.fused_compact) e = rpd::launch_compact(a, s);
+  if (e == hipSuccess && !a.fused_compact) e = rpd::launch_compact(a, lazy, s);
   if (e != hipSuccess) return fail(RPD_ERR_HIP, "compaction: %s", hipGetErrorString(e));
   if (p->max_masked < 0) {
     int32_t n = 0;

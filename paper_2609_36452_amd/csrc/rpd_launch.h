@@ -122,14 +122,15 @@ struct Launch {
 
 // enqueue, in this order: compaction, projection, reduction + scoring,
 // commitment (the last three use a.plan and a.max_masked)
-hipError_t launch_compact(const Launch& a, hipStream_t s);
+// lazy_list: also list the first lazy pass (a.lazy: act, rowoff, m, tier)
+hipError_t launch_compact(const Launch& a, bool lazy_list, hipStream_t s);
 hipError_t launch_projection(const Launch& a, hipStream_t s);
 hipError_t launch_reduce_score(const Launch& a, hipStream_t s);
 hipError_t launch_commit(const Launch& a, hipStream_t s);
 
-// lazy layerwise projection: list the rows of layer l (first: every position),
+// lazy layerwise projection: list the rows of layer l still walking,
 // reduce a pass over layer l, score from the per-position state
-hipError_t launch_lazy_next(const Launch& a, int l, int first, hipStream_t s);
+hipError_t launch_lazy_next(const Launch& a, int l, hipStream_t s);
 // nvt_class: the vocabulary-tile counts of the plans for rows <= 64, <= 128
 // and above, when the pass ran once per size class (NULL: a.plan's)
 hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, const int* nvt_class, hipStream_t s);

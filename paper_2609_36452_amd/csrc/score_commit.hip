@@ -10,10 +10,23 @@ namespace {
 
 // ------------------------------------------------------------ K0 compact --
 
+// With lazy projection the compaction also lists the first pass (the final
+// layer of every masked position, in order): act, the rows' element offsets,
+// the count and its size class (<= t0, <= t1, above) as k_lazy_next writes
+// them for the later passes.
+struct FirstPassList {
+  int32_t* act;          // NULL: no listing
+  long long* rowoff;
+  int32_t* m;
+  int32_t* tier;
+  long long layer_off;   // (K-1) * B * L: the final layer's first row
+  int d, t0, t1;
+};
+
 __global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ mask, int BL, int cap,
                                                    int32_t* __restrict__ rows, int32_t* __restrict__ n_out,
                                                    int32_t* __restrict__ dev_status,
-                                                   int32_t* __restrict__ user_status) {
+                                                   int32_t* __restrict__ user_status, FirstPassList fp) {
   __shared__ int wsum[16];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
   int carry = 0;
@@ -31,7 +44,13 @@ __global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ ma
       tot += c;
     }
     const int pos = carry + off + before;
-    if (f && pos < cap) rows[pos] = i;
+    if (f && pos < cap) {
+      rows[pos] = i;
+      if (fp.act) {
+        fp.act[pos] = pos;
+        fp.rowoff[pos] = (fp.layer_off + i) * fp.d;
+      }
+    }
     carry += tot;
     __syncthreads();
   }
@@ -44,6 +63,12 @@ __global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ ma
     *n_out = n;
     *dev_status = st;
     if (user_status) *user_status = st;
+    if (fp.act) {
+      *fp.m = n;
+      fp.tier[0] = n <= fp.t0 ? n : 0;
+      fp.tier[1] = n > fp.t0 && n <= fp.t1 ? n : 0;
+      fp.tier[2] = n > fp.t1 ? n : 0;
+    }
   }
 }
 
@@ -535,9 +560,13 @@ CommitArgs commit_args(const Launch& a) {
 
 }  // namespace
 
-hipError_t launch_compact(const Launch& a, hipStream_t s) {
+hipError_t launch_compact(const Launch& a, bool lazy_list, hipStream_t s) {
+  FirstPassList fp{};
+  if (lazy_list)
+    fp = FirstPassList{a.lazy.act, a.lazy.rowoff, a.lazy.m, a.lazy.tier, (long long)(a.K - 1) * a.B * a.L, a.d,
+                       kStreamMaxRows, kBigTileRowsMid};
   hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, a.mask, a.B * a.L, a.max_masked, a.rows, a.n_masked,
-                     a.dev_status, a.user_status);
+                     a.dev_status, a.user_status, fp);
   return hipGetLastError();
 }
 
