@@ -26,8 +26,9 @@ Every function follows a passage of the paper (He, Liu, Xiong, Zhang,
 * the RPD-block commitment -- Section 3.2 "Variants" and Appendix A.6
   "RPD-block": the candidates of the active 32-position block, no budget,
   fallback to the block's most confident masked position;
-* lazy layerwise projection -- Appendix A.6 "Layerwise projection": layers
-  are projected only until a position's agreement suffix is determined;
+* lazy layerwise projection -- Appendix A.6 "Layerwise projection": a
+  position's intermediate layers are projected from the final one down and
+  no further than its agreement suffix needs (the first disagreeing layer);
 * the end of an iteration (fill A_t with its predictions, keep the rest
   masked) and a loop of iterations until the canvas is filled -- Section 3.2.
 
@@ -79,6 +80,8 @@ class Params:
     block: int = 0           # 0: full RPD; > 0: RPD-block with blocks of this many positions
     logit_scale: float = 1.0  # multiplies every logit before the softmax statistics (1 / temperature)
     lazy: bool = False        # lazy layerwise projection (score_commit_lazy); the rule itself is unchanged
+    lazy_all: bool = False    # lazy: every masked position walks its layers (else only the band theta_c <= c < theta_h)
+    monotone: bool = False    # report-only reading of the agreement rule: see monotone_agreement (oracle only)
 
 
 LLADA = Params(theta_s=3.5, w=15.0)
@@ -242,6 +245,20 @@ def stability_score(k_i: int, r_i: float, p: Params) -> float:
     return float(min(k_i, p.k_max)) - p.w * r_i
 
 
+def monotone_agreement(layer_argmax: np.ndarray, p_final: np.ndarray) -> bool:
+    """The literal reading of the rule "argmax agreement across all K layers
+    with non-decreasing top probability": every layer predicts the final
+    token (K_i = K, Eq. 2) and that token's probability never falls from one
+    layer to the next. The reading the commit step implements instead is
+    Eq. 4 with w = 1, K_max >= K, theta_s = K (strict()): K_i = K and r_i <= 0
+    (Eq. 3), i.e. only the final layer has to hold the peak. This one is
+    evaluated by the oracle only, to report where the two readings part."""
+    K = len(layer_argmax)
+    if any(layer_argmax[l] != layer_argmax[K - 1] for l in range(K)):
+        return False
+    return all(p_final[l] <= p_final[l + 1] for l in range(K - 1))
+
+
 def candidate_routes(c: float, s: float, p: Params) -> tuple[bool, bool]:
     """Eq. (5): (high-confidence route, stability route). NaN fails both."""
     high = bool(c >= p.theta_h)
@@ -372,6 +389,8 @@ def select(mask: np.ndarray, layer: dict, p: Params, positions: list[tuple[int, 
             c_i = layer["conf"][a, K - 1]
             h_i = layer["entropy"][a, K - 1]
             high, stab = candidate_routes(c_i, s_i, p)
+            if p.monotone:   # the literal reading (report only): agreement with a non-decreasing probability
+                stab = bool(p.theta_c <= c_i < p.theta_h and monotone_agreement(am, pf))
             H[q], c[q], cand[q] = h_i, c_i, high or stab
             o["token"][b, i] = am[K - 1]
             o["entropy"][b, i] = h_i
@@ -405,14 +424,17 @@ def select(mask: np.ndarray, layer: dict, p: Params, positions: list[tuple[int, 
 
 def lazy_layer_stats(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params,
                      norm: tuple | None = None):
-    """Lazy layerwise projection (Appendix A.6 "Layerwise projection": layers
-    are materialized only until the agreement suffix of a position is
-    determined). The final layer of every masked position is projected first.
-    Only a position whose candidacy the stability test can decide
-    (theta_c <= c < theta_h, Eq. 5) projects intermediate layers, from K-2
-    downwards, stopping after the first layer whose argmax differs from the
-    final token; its persistence and drop are then exactly those of the eager
-    projection. Unprojected layers hold argmax -1 and NaN statistics.
+    """Lazy layerwise projection (Appendix A.6 "Layerwise projection"): the
+    final layer of every masked position is projected first; then a position
+    projects its intermediate layers from K-2 downwards, stopping after the
+    first layer whose argmax differs from the final token, which is where
+    its agreement suffix is known. Its persistence and drop are then exactly
+    those of the eager projection. With ``p.lazy_all`` every masked position
+    with a finite final confidence walks (the procedure as the paper states
+    it); otherwise only the positions whose candidacy the stability test
+    can decide (theta_c <= c < theta_h, Eq. 5) do, a further saving of this
+    implementation that leaves every decision unchanged. Unprojected layers
+    hold argmax -1 and NaN statistics.
     Returns (positions, per-layer statistics, layers projected per position)."""
     pos = masked_positions(mask)
     K = hidden.shape[0]
@@ -438,7 +460,7 @@ def lazy_layer_stats(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtyp
             layer[k][a, K - 1] = f[k]
         layer["p_final"][a, K - 1] = f["conf"]
         c = f["conf"]
-        if not (p.theta_c <= c < p.theta_h):
+        if not (_walks(c, p)):
             continue
         for l in range(K - 2, -1, -1):
             st = one(a, l)
@@ -450,18 +472,28 @@ def lazy_layer_stats(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtyp
     return pos, layer, projected
 
 
+def _walks(c: float, p: Params) -> bool:
+    """Whether a position with final confidence c walks its intermediate
+    layers in the lazy projection."""
+    if p.lazy_all:
+        return not np.isnan(c)
+    return bool(p.theta_c <= c < p.theta_h)
+
+
 def score_commit_lazy(hidden: np.ndarray, w_u: np.ndarray, mask: np.ndarray, dtype: str, p: Params,
                       norm: tuple | None = None) -> dict:
     """The commit step with lazy layerwise projection: the same candidacy and
     commitment as score_commit (stability matters only inside the band
-    theta_c <= c < theta_h, where the walk reaches the first disagreement).
-    Outside the band stability is not evaluated: persistence -1, drop and
-    stability NaN. ``layers_projected`` counts the projections per position."""
+    theta_c <= c < theta_h, and every walking position reaches its first
+    disagreement). Where a position does not walk (outside the band unless
+    ``p.lazy_all``; a NaN confidence) stability is not evaluated: persistence
+    -1, drop and stability NaN. ``layers_projected`` counts the projections
+    per position."""
     pos, layer, projected = lazy_layer_stats(hidden, w_u, mask, dtype, p, norm)
     o = assemble(mask, pos, layer, p)
     for a, (b, i) in enumerate(pos):
         c = layer["conf"][a, -1]
-        if not (p.theta_c <= c < p.theta_h):
+        if not _walks(c, p):
             o["persistence"][b, i] = -1
             o["drop"][b, i] = np.nan
             o["stability"][b, i] = np.nan

@@ -5,6 +5,7 @@ of the entropy (Eq. 1), an independent library entropy, hand-worked cases of
 Eq. (2)-(5), the drop ceilings printed in Appendix A.6, brute-force
 enumeration of the commitment fixed point of Section 3.2, and invariants of
 the rule (monotone budget, progress fallback)."""
+import dataclasses
 import itertools
 import json
 import math
@@ -187,6 +188,53 @@ def test_strict_rule_reading():
     assert O.stability_score(4, 0.0, P) >= P.theta_s
     assert O.stability_score(4, 1e-9, P) < P.theta_s
     assert O.stability_score(3, 0.0, P) < P.theta_s
+
+
+def _layer_case(ys, ps):
+    """Per-layer statistics of one masked position (argmax, top probability
+    of the final token) in the oracle's select() layout."""
+    ys, ps = np.asarray([ys]), np.asarray([ps], np.float64)
+    return {"argmax": ys, "conf": ps.copy(), "entropy": np.full(ps.shape, 0.1), "p_final": ps}
+
+
+@pytest.mark.parametrize("ys,ps,eq4,mono", [
+    ([7, 7, 7, 7], [0.62, 0.70, 0.80, 0.85], True, True),     # rising: both readings admit
+    ([7, 7, 7, 7], [0.62, 0.80, 0.70, 0.85], True, False),    # a dip before the final peak: Eq. 4 only
+    ([7, 7, 7, 7], [0.62, 0.70, 0.86, 0.85], False, False),   # the final layer below the peak: neither
+    ([7, 7, 7, 7], [0.85, 0.85, 0.85, 0.85], True, True),     # flat (non-decreasing)
+    ([3, 7, 7, 7], [0.62, 0.70, 0.80, 0.85], False, False),   # one layer disagrees: neither
+])
+def test_literal_monotone_reading_hand_cases(ys, ps, eq4, mono):
+    # the rule "agreement across all K layers with non-decreasing top probability": the commit step reads
+    # it as Eq. 4 (w = 1, theta_s = K: the final layer holds the peak, Eq. 3); the literal reading asks
+    # for a probability that never falls from layer to layer. Confidence 0.85 is inside the band.
+    mask = np.ones((1, 1), np.uint8)
+    P = O.strict(4, 1.0)
+    a = O.select(mask, _layer_case(ys, ps), P, [(0, 0)])
+    b = O.select(mask, _layer_case(ys, ps), dataclasses.replace(P, monotone=True), [(0, 0)])
+    assert bool(a["flags"][0, 0] & O.FLAG_STABLE) == eq4
+    assert bool(b["flags"][0, 0] & O.FLAG_STABLE) == mono
+    assert O.monotone_agreement(np.asarray(ys), np.asarray(ps)) == mono
+
+
+def test_literal_monotone_reading_split_on_the_tiny_workload():
+    # over seeded instances of the tiny fp32 workload (40 of 64 positions masked, K = 3): the literal
+    # reading admits a subset of what Eq. 4 admits (monotone => final layer is the peak => r_i = 0), and
+    # the two part on the positions whose probability dips before a final peak. Reported, not graded.
+    split_cand = split_commit = total = 0
+    for seed in range(40):
+        w = make_workload("tiny", seed)
+        P = O.strict(3, 1.0)
+        pos, layer = O.layer_stats_masked(w.hidden, w.w_u, w.mask, w.cfg.dtype)
+        a = O.assemble(w.mask, pos, layer, P)
+        b = O.assemble(w.mask, pos, layer, dataclasses.replace(P, monotone=True))
+        ca, cb = (a["flags"] & O.FLAG_CANDIDATE) > 0, (b["flags"] & O.FLAG_CANDIDATE) > 0
+        assert not (cb & ~ca).any()
+        split_cand += int((ca != cb).sum())
+        split_commit += int((a["commit"] != b["commit"]).sum())
+        total += int(w.mask.sum())
+    print(f"literal monotone vs Eq. 4 reading over 40 tiny instances: candidacy differs at {split_cand} "
+          f"and commitment at {split_commit} of {total} masked positions")
 
 
 # ------------------------------------------------------------ commitment --
@@ -542,8 +590,8 @@ def test_logit_scale_is_a_softmax_temperature():
 
 
 # ------------------------------------------------------- lazy projection ----
-# Appendix A.6 "Layerwise projection": layers are projected only until the
-# agreement suffix of a position is determined.
+# Appendix A.6 "Layerwise projection": the intermediate layers of a position
+# are projected lazily, from the final layer down to its first disagreement.
 
 @pytest.mark.parametrize("seed", range(6))
 @pytest.mark.parametrize("pname", ["llada", "dream"])
@@ -571,6 +619,29 @@ def test_lazy_projection_keeps_every_decision(seed, pname):
         want = min(K, eager["persistence"][b, i] + 1) if band[b, i] else 1
         assert lazy["layers_projected"][a] == want, (b, i)
     assert lazy["layers_projected"].sum() < K * len(pos)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_lazy_projection_walking_every_position(seed):
+    # lazy_all: every masked position walks its layers (the procedure without the band restriction), so
+    # persistence, drop and stability are reported everywhere and equal the eager projection's
+    cfg = CONFIGS["tiny"].with_(sharp=("calibrated",), unstable_frac=0.4)
+    w = make_workload(cfg, 320 + seed)
+    P = dataclasses.replace(O.DREAM, lazy=True, lazy_all=True)
+    eager = O.score_commit(w.hidden, w.w_u, w.mask, w.cfg.dtype, O.DREAM)
+    lazy = O.score_commit_lazy(w.hidden, w.w_u, w.mask, w.cfg.dtype, P)
+    m = w.mask != 0
+    for k in ("commit", "token", "flags", "n_commit", "persistence"):
+        np.testing.assert_array_equal(lazy[k], eager[k], err_msg=k)
+    for k in ("entropy", "confidence", "upstream_entropy", "drop", "stability"):
+        np.testing.assert_allclose(lazy[k][m], eager[k][m], rtol=1e-12, atol=1e-12, err_msg=k)
+    pos = O.masked_positions(w.mask)
+    K = w.cfg.K
+    for a, (b, i) in enumerate(pos):
+        assert lazy["layers_projected"][a] == min(K, eager["persistence"][b, i] + 1), (b, i)
+    # the band-only walk projects no more layers than the full one
+    band = O.score_commit_lazy(w.hidden, w.w_u, w.mask, w.cfg.dtype, dataclasses.replace(P, lazy_all=False))
+    assert band["layers_projected"].sum() <= lazy["layers_projected"].sum()
 
 
 def test_lazy_projection_with_normalization():
