@@ -29,7 +29,11 @@ def to_device(w, dev="cuda:0"):
 
 
 def gpu_params(P: O.Params) -> rpd.Params:
-    return rpd.Params(**dataclasses.asdict(P))
+    """The oracle's parameters as the binding's (the literal monotone reading
+    exists in the oracle only, for reporting)."""
+    assert not P.monotone, "the monotone reading is an oracle-only report"
+    fields = rpd.Params.__dataclass_fields__
+    return rpd.Params(**{k: v for k, v in dataclasses.asdict(P).items() if k in fields})
 
 
 def gain_tensor(w, g: np.ndarray, dev="cuda:0") -> torch.Tensor:
