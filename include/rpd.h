@@ -22,9 +22,13 @@
  *  - Arrays are dense and row-major in the shapes given. The final layer of
  *    the window is layer K-1.
  *  - Errors: every argument is validated on the host before anything is
- *    enqueued; on a non-OK status nothing was enqueued and the outputs are
- *    untouched. rpd_last_error() then describes the failure (thread-local).
- *    No C++ exception crosses this interface.
+ *    enqueued, so a status other than RPD_OK and RPD_ERR_HIP means nothing
+ *    was enqueued and the outputs are untouched. RPD_ERR_HIP reports a HIP
+ *    runtime call or launch that failed part-way: the work enqueued before
+ *    it stays enqueued and may have written the outputs and the workspace
+ *    in part, so the outputs are then undefined (and the stream may be in
+ *    an error state, as HIP reports it). rpd_last_error() describes the
+ *    failure (thread-local). No C++ exception crosses this interface.
  *  - Calls on distinct streams with distinct workspaces may overlap.
  */
 #ifndef RPD_H
@@ -37,7 +41,7 @@
 extern "C" {
 #endif
 
-#define RPD_ABI_VERSION 2
+#define RPD_ABI_VERSION 3
 
 /* element type of `hidden` and `w_u` (both must have the same type) */
 enum { RPD_DTYPE_BF16 = 0, RPD_DTYPE_F32 = 1 };
@@ -53,7 +57,8 @@ typedef enum rpd_status {
 } rpd_status;
 
 /* bits of rpd_params.flags */
-#define RPD_PARAM_LAZY 1u /* lazy layerwise projection (see rpd_params) */
+#define RPD_PARAM_LAZY 1u     /* lazy layerwise projection (see rpd_params) */
+#define RPD_PARAM_LAZY_ALL 2u /* with RPD_PARAM_LAZY: every masked position walks its layers */
 
 /* per-position flag bits written to rpd_outputs.flags */
 #define RPD_FLAG_CANDIDATE 1u  /* in the candidate set C_t (Eq. 5) */
@@ -119,8 +124,8 @@ typedef struct rpd_problem {
  * Hyperparameters (Table 4, Appendix A.6; LLaDA: theta_s 3.5, w 15; Dream:
  * theta_s 2.5, w 20; both theta_h 0.9, theta_c 0.6, K_max 6, beta 4 nats,
  * W 32). Requirements: 0 <= theta_c <= theta_h, w >= 0, k_max >= 1,
- * beta >= 0 (may be +inf), window >= 1, flags only RPD_PARAM_LAZY,
- * block >= 0; no NaN.
+ * beta >= 0 (may be +inf), window >= 1, flags only RPD_PARAM_LAZY and
+ * RPD_PARAM_LAZY_ALL (the latter only with the former), block >= 0; no NaN.
  *
  * block selects the commitment rule. 0: full RPD (Section 3.2), the
  * cumulative-entropy budget beta over the whole canvas with the fallback
@@ -134,15 +139,21 @@ typedef struct rpd_problem {
  * positions outside the commitment set.
  *
  * RPD_PARAM_LAZY in flags: lazy layerwise projection (Appendix A.6
- * "Layerwise projection": layers are projected only until a position's
- * agreement suffix is determined). The final layer of every masked position
- * is projected first; intermediate layers only for positions with
- * theta_c <= c < theta_h (the only ones whose candidacy stability decides,
- * Eq. 5), from layer K-2 down, each stopping after its first disagreeing
- * layer. Tokens, candidacy and commitment are those of the eager projection,
- * and so are persistence, drop and stability inside that band; outside it
- * they are not evaluated (persistence -1, drop and stability NaN), and the
- * per-layer outputs of layers never projected hold -1 / NaN. One projection
+ * "Layerwise projection": a position's intermediate layers are projected
+ * from the final one down, no further than its agreement suffix needs). The
+ * final layer of every masked position is projected first; then the
+ * positions that walk project layer K-2, K-3, ..., each stopping after its
+ * first disagreeing layer. With RPD_PARAM_LAZY_ALL as well, every masked
+ * position with a finite final confidence walks (the procedure as the paper
+ * states it), and persistence, drop and stability equal the eager
+ * projection's everywhere. Without it only the positions with
+ * theta_c <= c < theta_h walk: the only ones whose candidacy the stability
+ * test decides (Eq. 5), a further saving of this library beyond the
+ * paper's procedure that leaves every decision unchanged; outside that band
+ * persistence, drop and stability are then not evaluated (persistence -1,
+ * drop and stability NaN). Either way tokens, candidacy and commitment are
+ * those of the eager projection, and the per-layer outputs of layers never
+ * projected hold -1 / NaN. One projection
  * pass per layer (each streams W_U again): it pays where the projection is
  * compute-bound (many masked positions), not where streaming W_U dominates.
  * While the bound on a pass's rows (max_masked, then the last count read

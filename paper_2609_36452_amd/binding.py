@@ -26,6 +26,7 @@ FLAG_FALLBACK = 16
 
 DEVICE_STATUS_MASKED_OVERFLOW = 1
 PARAM_LAZY = 1
+PARAM_LAZY_ALL = 2
 
 STATUS_NAMES = {0: "RPD_OK", 1: "RPD_ERR_NULL_POINTER", 2: "RPD_ERR_BAD_SHAPE", 3: "RPD_ERR_BAD_PARAM",
                 4: "RPD_ERR_WORKSPACE_TOO_SMALL", 5: "RPD_ERR_UNSUPPORTED", 6: "RPD_ERR_HIP"}
@@ -67,6 +68,7 @@ class Params:
     block: int = 0     # 0: full RPD; > 0: RPD-block with blocks of this many positions
     logit_scale: float = 1.0   # inverse temperature of the scoring softmax
     lazy: bool = False         # lazy layerwise projection (RPD_PARAM_LAZY)
+    lazy_all: bool = False     # with lazy: every masked position walks its layers (RPD_PARAM_LAZY_ALL)
 
     @staticmethod
     def llada() -> "Params":
@@ -83,9 +85,9 @@ class Params:
         return Params(theta_s=float(K), w=1.0, k_max=max(K, 6), beta=beta)
 
     def to_c(self) -> RpdParams:
+        flags = (PARAM_LAZY if self.lazy else 0) | (PARAM_LAZY_ALL if self.lazy_all else 0)
         return RpdParams(self.theta_h, self.theta_c, self.theta_s, self.w, int(self.k_max), self.beta,
-                         int(self.window), PARAM_LAZY if self.lazy else 0, int(self.block),
-                         float(self.logit_scale))
+                         int(self.window), flags, int(self.block), float(self.logit_scale))
 
 
 class RpdError(RuntimeError):

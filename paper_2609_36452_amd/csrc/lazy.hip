@@ -1,13 +1,17 @@
-// Lazy layerwise projection (Appendix A.6 "Layerwise projection": layers are
-// materialized only until the agreement suffix of a position is determined).
+// Lazy layerwise projection (Appendix A.6 "Layerwise projection"): a
+// position's intermediate layers are projected from the final one down, and
+// no further than its first disagreeing layer, where its agreement suffix
+// (Eq. 2) is known.
 //
 // The host drives one pass per layer, from the final layer down:
 //   pass 0      the final layer of every masked position;
-//   pass t > 0  layer K-1-t of the positions still "alive": those whose
-//               final confidence lies in the band theta_c <= c < theta_h
-//               (the only ones whose candidacy the stability test decides,
-//               Eq. 5) and whose layers K-t .. K-1 all agreed with the final
-//               token.
+//   pass t > 0  layer K-1-t of the positions still "alive": those that walk
+//               (every position with a finite final confidence with
+//               RPD_PARAM_LAZY_ALL, the procedure as the paper states it;
+//               otherwise only those in the band theta_c <= c < theta_h, the
+//               only ones whose candidacy the stability test decides, Eq. 5,
+//               a further saving that leaves every decision unchanged) and
+//               whose layers K-t .. K-1 all agreed with the final token.
 // Each pass is the ordinary projection over an explicit list of rows (a
 // table of element offsets into the hidden states, or normalized rows),
 // followed by k_lazy_reduce (merge the tile states, update each position's
@@ -15,37 +19,24 @@
 // still alive with the row offsets of the next layer, and their count; the
 // host plans the next pass for a bound on it or reads it back). k_lazy_score then
 // evaluates Eq. 2-5 from the per-position state, with persistence exact for
-// every position of the band; outside it stability is not evaluated
+// every position that walked; elsewhere stability is not evaluated
 // (persistence -1, drop and stability NaN). The commitment follows as usual.
-#include "rpd_device.h"
+#include "reduce_device.h"
 
 namespace rpd {
 namespace {
 
-// fixed-order merge of one row's nvt tile states by one wave (as the eager
-// reduction does)
-__device__ __forceinline__ Soft lazy_merge_row(const float4* __restrict__ src, int nvt, int lane) {
-  const float4 empty = soft_pack(soft_empty());
-  Soft s = soft_empty();
-  for (int t0 = lane; t0 < nvt; t0 += 64 * 8) {
-    float4 v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = (t0 + 64 * u < nvt) ? src[t0 + 64 * u] : empty;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) s = soft_merge(s, soft_unpack(v[u]));
-  }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) s = soft_merge(s, soft_shfl_xor(s, m));
-  return s;
-}
-
-// one wave per row j < m of the pass (layer l): statistics of the row, then
-// the update of its position's state
+// one wave per row j < m of the pass (layer l): statistics of the row (with
+// exact argmax ties resolved after a streaming projection, whose tiles sum
+// in different orders: bit c of tie_cls for size class c), then the update
+// of its position's state
 __global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ partials, int nvt0, int nvt1,
-                                                    int nvt2, int t0, int t1,
+                                                    int nvt2, int t0, int t1, TieArgs ta, int tie_cls,
+                                                    const uint16_t* __restrict__ hidden,
+                                                    const uint16_t* __restrict__ xrows, int d,
                                                     const int32_t* __restrict__ m_ptr, LazyState st, int l, int K,
                                                     int B, int L, const int32_t* __restrict__ rows, float theta_c,
-                                                    float theta_h, int32_t* __restrict__ layer_argmax,
+                                                    float theta_h, int walk_all, int32_t* __restrict__ layer_argmax,
                                                     float* __restrict__ layer_conf, float* __restrict__ layer_entropy) {
   const int j = blockIdx.x, lane = threadIdx.x;
   // the row's position is loaded with the count (j < m_cap stays inside act),
@@ -58,11 +49,18 @@ __global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ p
   if (j >= m) return;
   // the partials follow the plan of the size class the count is in (<= t0,
   // <= t1, above; one plan when the pass was launched once)
-  const int nvt = m <= t0 ? nvt0 : (m <= t1 ? nvt1 : nvt2);
+  const int cls = m <= t0 ? 0 : (m <= t1 ? 1 : 2);
+  const int nvt = cls == 0 ? nvt0 : (cls == 1 ? nvt1 : nvt2);
   const int y_prev = st.y[p], k_prev = st.k[p];
   const float pmax_prev = st.pmax[p];
   const int pos = layer_argmax ? rows[p] : 0;
-  const Soft s = lazy_merge_row(partials + (long long)j * nvt, nvt, lane);
+  const float4* src = partials + (long long)j * nvt;
+  float4 keep[8];
+  Soft s = wave_merge_row(src, nvt, lane, keep);
+  if ((tie_cls >> cls) & 1) {
+    const uint16_t* x = xrows ? xrows + (long long)j * d : hidden + st.rowoff[j];
+    s.idx = resolve_tie(s, keep, src, nvt, ta, x, lane);
+  }
   if (lane != 0) return;
   const int y = (s.idx == INT_MAX) ? -1 : s.idx;
   const float c = 1.0f / s.S;
@@ -73,7 +71,8 @@ __global__ __launch_bounds__(64) void k_lazy_reduce(const float4* __restrict__ p
     st.h[p] = h;
     st.k[p] = 1;
     st.pmax[p] = c;
-    st.alive[p] = (K > 1 && c >= theta_c && c < theta_h) ? 1 : 0;   // NaN fails
+    // NaN fails both tests
+    st.alive[p] = (K > 1 && (walk_all ? c == c : (c >= theta_c && c < theta_h))) ? 1 : 0;
   } else if (y == y_prev) {
     st.k[p] = k_prev + 1;
     st.pmax[p] = fmaxf(pmax_prev, c);
@@ -153,15 +152,16 @@ __global__ __launch_bounds__(256) void k_lazy_score(const int32_t* __restrict__ 
   const long long o = (long long)b * a.L + i;
   const float c = st.c[p];
   const bool band = c >= a.theta_c && c < a.theta_h;
+  const bool walked = a.walk_all ? c == c : band;
   const bool high = c >= a.theta_h;
   float r = NAN, s = NAN;
   int k = -1;
   bool stab = false;
-  if (band) {
+  if (walked) {
     k = st.k[p];
     r = st.pmax[p] - c;
     s = fmaf(-a.w, r, (float)min(k, a.k_max));
-    stab = s >= a.theta_s;
+    stab = band && s >= a.theta_s;
   }
   a.token[o] = st.y[p];
   a.entropy[o] = st.h[p];
@@ -187,21 +187,28 @@ hipError_t launch_lazy_next(const Launch& a, int l, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, const int* nvt_class, hipStream_t s) {
+hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, const ProjPlan* class_plans, hipStream_t s) {
   if (m_cap <= 0) return hipSuccess;
-  const int n0 = nvt_class ? nvt_class[0] : a.plan.nvt, n1 = nvt_class ? nvt_class[1] : a.plan.nvt,
-            n2 = nvt_class ? nvt_class[2] : a.plan.nvt;
-  hipLaunchKernelGGL(k_lazy_reduce, dim3(m_cap), dim3(64), 0, s, a.partials, n0, n1, n2, kStreamMaxRows,
-                     kBigTileRowsMid, a.n_masked, a.lazy, l, a.K,
-                     a.B, a.L, a.rows, a.theta_c, a.theta_h, a.layer_argmax, a.layer_conf, a.layer_entropy);
+  const ProjPlan* pl[3] = {&a.plan, &a.plan, &a.plan};
+  if (class_plans)
+    for (int c = 0; c < 3; ++c) pl[c] = class_plans + c;
+  int tie_cls = 0;
+  for (int c = 0; c < 3; ++c) tie_cls |= tie_args(a, *pl[c]).w_u ? 1 << c : 0;
+  const TieArgs ta{static_cast<const uint16_t*>(a.w_u), a.d, a.logit_scale};
+  hipLaunchKernelGGL(k_lazy_reduce, dim3(m_cap), dim3(64), 0, s, a.partials, pl[0]->nvt, pl[1]->nvt, pl[2]->nvt,
+                     kStreamMaxRows, kBigTileRowsMid, ta, tie_cls, static_cast<const uint16_t*>(a.hidden),
+                     static_cast<const uint16_t*>(a.xrows), a.d, a.n_masked, a.lazy, l, a.K,
+                     a.B, a.L, a.rows, a.theta_c, a.theta_h, a.lazy_all ? 1 : 0, a.layer_argmax, a.layer_conf,
+                     a.layer_entropy);
   return hipGetLastError();
 }
 
 hipError_t launch_lazy_score(const Launch& a, hipStream_t s) {
   if (a.max_masked <= 0) return hipSuccess;
   LazyScoreArgs sa{a.K,          a.B,          a.L,         a.theta_h,     a.theta_c,    a.theta_s,
-                   a.w,          a.k_max,      a.token,     a.entropy,     a.confidence, a.persistence,
-                   a.drop,       a.stability,  a.flags,     a.layer_argmax, a.layer_conf, a.layer_entropy};
+                   a.w,          a.k_max,      a.lazy_all ? 1 : 0,        a.token,      a.entropy,
+                   a.confidence, a.persistence, a.drop,     a.stability,   a.flags,      a.layer_argmax,
+                   a.layer_conf, a.layer_entropy};
   hipLaunchKernelGGL(k_lazy_score, dim3((unsigned)((a.max_masked + 255) / 256)), dim3(256), 0, s, a.n_masked,
                      a.lazy, a.rows, sa);
   return hipGetLastError();

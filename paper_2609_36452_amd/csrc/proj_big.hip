@@ -231,16 +231,16 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     __builtin_amdgcn_sched_barrier(0);                                                                    \
   } while (0)
 
-  // Chunks past the end repeat the last one (loaded, never multiplied). With a
-  // single row tile (NT) full chunks are taken in the order rot, rot+1, ..,
-  // nchf-1, 0, .., rot-1: requests in flight on different vocabulary tiles
-  // then read different columns of W_U (in plain order they crowded onto a
-  // few HBM channels). With several row tiles the plain order stays: the
-  // workgroups of one row tile share its hidden rows through L2 only while
-  // they read the same chunk (rotated, 7-8% slower at 1024 rows and up).
+  // Chunks past the end repeat the last one (loaded, never multiplied). Every
+  // tile takes the chunks in plain order, so every vocabulary row's products
+  // are summed the same way and equal W_U rows give bit-identical logits (an
+  // exact tie goes to the lowest index). Starting each tile at its own chunk,
+  // as the streaming kernel does against HBM channel crowding, measured
+  // neutral here with a single row tile and 7-8% slower from 1024 rows up,
+  // where the workgroups of one row tile share its hidden rows through L2
+  // only while they read the same chunk.
   const int nchf = d / KC;
-  const int rot = NT && nchf > 0 ? (int)((7ll * vt) % nchf) : 0;
-#define RPD_PCHUNK(c) ((c) + rot >= nchf ? (c) + rot - nchf : (c) + rot)
+#define RPD_PCHUNK(c) (c)
   if (nchf > 0) {
     RPD_ALOAD(0, 0);
     RPD_BLOAD(0, 0);

@@ -81,8 +81,11 @@ rpd_status check_params(const rpd_params* q) {
   if (q->k_max < 1) return fail(RPD_ERR_BAD_PARAM, "k_max must be >= 1 (got %d)", q->k_max);
   if (std::isnan(q->beta) || q->beta < 0.f) return fail(RPD_ERR_BAD_PARAM, "beta must be >= 0 (got %g)", q->beta);
   if (q->window < 1) return fail(RPD_ERR_BAD_PARAM, "window must be >= 1 (got %d)", q->window);
-  if (q->flags & ~(uint32_t)RPD_PARAM_LAZY)
-    return fail(RPD_ERR_BAD_PARAM, "flags holds unknown bits (0x%x); only RPD_PARAM_LAZY is defined", q->flags);
+  if (q->flags & ~(uint32_t)(RPD_PARAM_LAZY | RPD_PARAM_LAZY_ALL))
+    return fail(RPD_ERR_BAD_PARAM, "flags holds unknown bits (0x%x); RPD_PARAM_LAZY and RPD_PARAM_LAZY_ALL are defined",
+                q->flags);
+  if ((q->flags & RPD_PARAM_LAZY_ALL) && !(q->flags & RPD_PARAM_LAZY))
+    return fail(RPD_ERR_BAD_PARAM, "RPD_PARAM_LAZY_ALL needs RPD_PARAM_LAZY");
   if (q->block < 0) return fail(RPD_ERR_BAD_PARAM, "block must be >= 0 (got %d)", q->block);
   if (!std::isfinite(q->logit_scale) || q->logit_scale < 0.f)
     return fail(RPD_ERR_BAD_PARAM, "logit_scale must be finite and > 0, or 0 for 1 (got %g)", q->logit_scale);
@@ -110,6 +113,7 @@ void fill_common(rpd::Launch& a, const rpd_params* q, const rpd_outputs* o) {
   a.window = q->window;
   a.block = q->block;
   a.logit_scale = q->logit_scale == 0.f ? 1.f : q->logit_scale;
+  a.lazy_all = (q->flags & RPD_PARAM_LAZY_ALL) != 0;
   a.commit = o->commit;
   a.token = o->token;
   a.entropy = o->entropy;
@@ -179,13 +183,13 @@ hipError_t run_lazy(rpd::Launch& a, int dtype, hipStream_t s, Mark& mark) {
       } else {
         const int caps[3] = {rpd::kStreamMaxRows, std::min(m_host, rpd::kBigTileRowsMid), m_host};
         const int ncls = m_host > rpd::kBigTileRowsMid ? 3 : 2;
-        int nvt[3];
+        rpd::ProjPlan plans[3];
         for (int c = 0; c < 3; ++c) {
           const rpd::Launch ap = pass_launch(l, a.lazy.tier + c, caps[c]);
-          nvt[c] = ap.plan.nvt;
+          plans[c] = ap.plan;
           if (c < ncls && (e = rpd::launch_projection(ap, s)) != hipSuccess) return e;
         }
-        if ((e = rpd::launch_lazy_reduce(whole, l, m_host, nvt, s)) != hipSuccess) return e;
+        if ((e = rpd::launch_lazy_reduce(whole, l, m_host, plans, s)) != hipSuccess) return e;
       }
       if (l > 0 && (e = rpd::launch_lazy_next(a, l - 1, s)) != hipSuccess) return e;
     }

@@ -70,6 +70,7 @@ struct LazyScoreArgs {
   int K, B, L;
   float theta_h, theta_c, theta_s, w;
   int k_max;
+  int walk_all;        // every position with a finite confidence walked (else only the band)
   int32_t* token;
   float* entropy;
   float* confidence;
@@ -112,6 +113,7 @@ struct Launch {
   int k_max, window;
   int block;             // 0: full RPD; > 0: RPD-block
   float logit_scale;     // multiplies every logit before the softmax statistics
+  bool lazy_all;         // lazy projection: every masked position walks its layers (RPD_PARAM_LAZY_ALL)
   // outputs
   uint8_t* commit; int32_t* token; float* entropy; float* confidence;
   int32_t* persistence; float* drop; float* stability; uint8_t* flags;
@@ -131,9 +133,9 @@ hipError_t launch_commit(const Launch& a, hipStream_t s);
 // lazy layerwise projection: list the rows of layer l still walking,
 // reduce a pass over layer l, score from the per-position state
 hipError_t launch_lazy_next(const Launch& a, int l, hipStream_t s);
-// nvt_class: the vocabulary-tile counts of the plans for rows <= 64, <= 128
-// and above, when the pass ran once per size class (NULL: a.plan's)
-hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, const int* nvt_class, hipStream_t s);
+// class_plans: the plans for rows <= 64, <= 128 and above, when the pass
+// ran once per size class (NULL: a.plan)
+hipError_t launch_lazy_reduce(const Launch& a, int l, int m_cap, const ProjPlan* class_plans, hipStream_t s);
 hipError_t launch_lazy_score(const Launch& a, hipStream_t s);
 // the projection does the compaction itself (needs a.plan and a.max_masked
 // >= 0): the call then launches no compaction kernel

@@ -3,7 +3,7 @@
 // progress fallback (Section 3.2), and their launchers.
 #include <algorithm>
 
-#include "rpd_device.h"
+#include "reduce_device.h"
 
 namespace rpd {
 namespace {
@@ -106,25 +106,6 @@ struct ScoreArgs {
 // xor butterfly combines the lanes. Wave 0 then evaluates persistence, drop
 // and stability with one lane per layer.
 constexpr int kReduceWaves = 4;
-
-// Fixed-order merge of one row's nvt vocabulary-tile states by one wave:
-// lane folds tiles lane, lane+64, ... in tile order (loads batched eight at
-// a time: one round trip for up to 512 tiles), then an xor butterfly
-// combines the lanes. Every lane returns the row's state.
-__device__ __forceinline__ Soft wave_merge_row(const float4* __restrict__ src, int nvt, int lane) {
-  const float4 empty = soft_pack(soft_empty());
-  Soft s = soft_empty();
-  for (int t0 = lane; t0 < nvt; t0 += 64 * 8) {
-    float4 v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = (t0 + 64 * u < nvt) ? src[t0 + 64 * u] : empty;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) s = soft_merge(s, soft_unpack(v[u]));
-  }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) s = soft_merge(s, soft_shfl_xor(s, m));
-  return s;
-}
 
 // argmax (-1 if none), top probability 1/S and entropy ln S - T/S (Eq. 1) of
 // a merged state; NaN stays visible in the entropy
@@ -408,8 +389,10 @@ __global__ __launch_bounds__(kCommitThreads) void k_commit(const uint8_t* __rest
 }
 
 // K2: one workgroup of four waves per masked position. Wave w merges the
-// vocab-tile states of layers w, w+4, ... (wave_merge_row); wave 0 then
-// evaluates persistence, drop and stability with one lane per layer. The
+// vocab-tile states of layers w, w+4, ... (wave_merge_row) and, after a
+// projection whose tiles sum in different orders, resolves exact argmax
+// ties (resolve_tie; ta.w_u NULL otherwise); wave 0 then evaluates
+// persistence, drop and stability with one lane per layer. The
 // commitment (K3) follows as its own launch: handing it to the last
 // workgroup to finish instead needs a device-scope release and acquire in
 // every workgroup (an L2 write-back and invalidate each), which measured
@@ -417,7 +400,9 @@ __global__ __launch_bounds__(kCommitThreads) void k_commit(const uint8_t* __rest
 __global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4* __restrict__ partials,
                                                                      const int32_t* __restrict__ rows,
                                                                      const int32_t* __restrict__ n_ptr, int nvt,
-                                                                     ScoreArgs a) {
+                                                                     ScoreArgs a, TieArgs ta,
+                                                                     const uint16_t* __restrict__ hidden,
+                                                                     const uint16_t* __restrict__ xrows, int d) {
   __shared__ int ly[64];
   __shared__ float lc[64], lh[64];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -431,7 +416,14 @@ __global__ __launch_bounds__(64 * kReduceWaves) void k_reduce_score(const float4
     const int pos = rows[p];
     const int b = pos / a.L, i = pos - b * a.L;
     for (int l = wid; l < a.K; l += kReduceWaves) {
-      const Soft s = wave_merge_row(partials + ((long long)p * a.K + l) * nvt, nvt, lane);
+      const float4* src = partials + ((long long)p * a.K + l) * nvt;
+      float4 keep[8];
+      Soft s = wave_merge_row(src, nvt, lane, keep);
+      if (ta.w_u && p < n) {   // rows past the count are not valid (and never read)
+        const uint16_t* x = xrows ? xrows + ((long long)p * a.K + l) * d
+                                  : hidden + (((long long)l * a.B + b) * a.L + i) * (long long)d;
+        s.idx = resolve_tie(s, keep, src, nvt, ta, x, lane);
+      }
       if (lane == 0) state_stats(s, ly[l], lc[l], lh[l]);
     }
     if (p >= n) return;
@@ -573,7 +565,8 @@ hipError_t launch_compact(const Launch& a, bool lazy_list, hipStream_t s) {
 hipError_t launch_reduce_score(const Launch& a, hipStream_t s) {
   if (a.max_masked <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_reduce_score, dim3(a.max_masked), dim3(64 * kReduceWaves), 0, s, a.partials, a.rows,
-                     a.n_masked, a.plan.nvt, score_args(a));
+                     a.n_masked, a.plan.nvt, score_args(a), tie_args(a, a.plan), static_cast<const uint16_t*>(a.hidden),
+                     static_cast<const uint16_t*>(a.xrows), a.d);
   return hipGetLastError();
 }
 

@@ -40,7 +40,7 @@ def test_struct_layouts():
 
 
 def test_version_and_status_strings():
-    assert rpd.abi_version() == 2
+    assert rpd.abi_version() == 3
     assert rpd.status_string(0) == "ok"
     assert rpd.status_string(4) == "workspace too small"
 
@@ -129,7 +129,7 @@ def test_problem_validation(kw, status):
 
 
 @pytest.mark.parametrize("kw", [dict(theta_c=0.95), dict(theta_c=-0.1), dict(w=-1.0), dict(k_max=0),
-                                dict(beta=-1.0), dict(beta=math.nan), dict(window=0), dict(flags=2),
+                                dict(beta=-1.0), dict(beta=math.nan), dict(window=0), dict(flags=2), dict(flags=4), dict(flags=7),
                                 dict(theta_h=math.nan), dict(theta_s=math.inf), dict(block=-1),
                                 dict(logit_scale=-1.0), dict(logit_scale=math.inf)])
 def test_param_validation(kw):

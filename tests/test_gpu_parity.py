@@ -6,9 +6,12 @@ vocabulary sizes and hidden sizes that are not multiples of the 64-wide
 k-chunk, and every projection variant (the streaming family at <= 32 and
 64 projected rows, and the 128-, 192- and 256-row MFMA tiles above, with row
 tiles split across XCDs, and rows gathered through 32-bit buffer offsets or,
-from a hidden tensor of more than 2^31 bytes, 64-bit addresses). Full-size LLaDA-8B / Dream-7B shapes are
-compared on sampled positions that the oracle computes one by one, plus the
-prefix-sum identity of the commitment on the GPU's own outputs."""
+from a hidden tensor of more than 2^31 bytes, 64-bit addresses). The
+full-size LLaDA-8B / Dream-7B shapes are compared at every masked position
+and layer too (whole sequences of the batched shapes), and additionally on
+sampled positions of the whole batches. Edge cases: exact argmax ties from
+duplicated unembedding rows, zero hidden rows (uniform distribution), empty
+sequences inside a batch, NaN rows, budget and window extremes."""
 import dataclasses
 import math
 
@@ -190,6 +193,25 @@ def test_lazy_projection(name, ov, seed):
         assert (g["persistence"][m & ~band] == -1).all() and np.isnan(g["stability"][m & ~band]).all()
 
 
+@pytest.mark.parametrize("name,ov,seed", LAZY_CASES, ids=[c[0] for c in LAZY_CASES])
+def test_lazy_projection_walking_every_position(name, ov, seed):
+    # RPD_PARAM_LAZY_ALL: every masked position walks its layers down to its first disagreement (the
+    # procedure of Appendix A.6 without the band restriction): persistence, drop and stability are
+    # reported at every position and equal the eager projection's
+    base = CONFIGS["llada_late"].with_(name="lazyall_" + name, sharp=("calibrated",), unstable_frac=0.4).with_(**ov)
+    w = make_workload(base, seed)
+    for P in (dataclasses.replace(O.LLADA, lazy=True, lazy_all=True),
+              dataclasses.replace(O.DREAM, lazy=True, lazy_all=True, block=32)):
+        g, o, _ = _check(w, P)
+        eager = run_gpu(w, dataclasses.replace(P, lazy=False, lazy_all=False))
+        m = w.mask != 0
+        np.testing.assert_array_equal(g["token"][m], eager["token"][m])
+        same = m & (g["persistence"] == eager["persistence"])
+        assert same.sum() >= m.sum() - 2
+        assert (g["persistence"][m] >= 1).all()
+        assert np.abs(g["drop"][same] - eager["drop"][same]).max(initial=0.0) <= 2 * CONF_TOL
+
+
 def test_lazy_projection_with_normalization_and_fp32():
     w = make_workload(CONFIGS["tiny"].with_(sharp=("calibrated",), unstable_frac=0.4), 8)
     _check(w, dataclasses.replace(O.LLADA, lazy=True), norm=(_gain(w, 3), 1e-6, False))
@@ -218,6 +240,93 @@ def test_no_masked_positions():
     assert (g["commit"] == 0).all() and (g["token"] == -1).all() and (g["n_commit"] == 0).all()
     g = run_gpu(w, O.LLADA, max_masked=-1)
     assert (g["commit"] == 0).all() and (g["n_commit"] == 0).all()
+
+
+def test_empty_sequences_between_nonempty_ones():
+    # sequences 1 and 3 of five have no masked position: they commit nothing while their neighbours do
+    w = _small_bf16(seed=11, B=5, L=48, n_masked=12)
+    for b in (1, 3):
+        w.mask[b] = 0
+        w.hidden[:, b] = np.uint16(0x7FC0)
+    for P in (O.LLADA, O.strict(4, 0.5), O.Params(theta_s=3.5, w=15.0, block=32),
+              O.Params(beta=0.0, theta_h=0.999999, theta_c=0.999998)):
+        g, o, _ = _check(w, P, max_masked=int(w.mask.sum()))
+        assert g["n_commit"][1] == 0 and g["n_commit"][3] == 0
+        assert (g["n_commit"][[0, 2, 4]] >= 1).all()
+    # also through the read-back of the count and the bound covering the whole canvas
+    _check(w, O.LLADA, max_masked=-1)
+    _check(w, O.LLADA, max_masked=w.cfg.B * w.cfg.L)
+
+
+DUP_CASES = [  # name, overrides (rows = K * masked decide the projection variant)
+    ("bf16_s32", dict(B=1, L=64, K=4, d=264, V=5003, n_masked=8)),
+    ("bf16_s64", dict(B=2, L=40, K=3, d=512, V=4099, n_masked=10)),
+    ("bf16_big128", dict(B=2, L=40, K=4, d=520, V=7001, n_masked=12)),
+    ("bf16_big", dict(B=1, L=80, K=3, d=200, V=6007, n_masked=80)),
+    ("bf16_big_row_split", dict(B=2, L=256, K=4, d=136, V=30011, n_masked=None, masked_frac=1.0)),
+    ("f32", dict(B=1, L=64, K=3, d=256, V=4096, n_masked=40, dtype="f32")),
+    # more than 512 vocabulary tiles (768): the tie check reads the tile states past the first 512 again
+    ("bf16_s32_768_tiles", dict(B=1, L=64, K=4, d=128, V=140001, n_masked=8)),
+]
+
+
+def _duplicate_rows(w, shifts):
+    """Copy the unembedding row of every layer's target token to the rows
+    `t + s` (mod V) for each shift s, so that the top logit is an exact tie
+    (gap 0) between the target and its copies: the lowest index must win."""
+    w.w_u = w.w_u.copy()   # the cached matrix stays intact
+    V = w.cfg.V
+    pos = O.masked_positions(w.mask)
+    st = O.project_layer_stats(w.hidden, w.w_u, w.cfg.dtype, pos)
+    tops = sorted({int(t) for t in st["argmax"].ravel()})
+    for t in tops:
+        for s in shifts:
+            u = (t + s) % V
+            if u not in tops:
+                w.w_u[u] = w.w_u[t]
+    return tops
+
+
+@pytest.mark.parametrize("name,ov", DUP_CASES, ids=[c[0] for c in DUP_CASES])
+@pytest.mark.parametrize("where", ["near", "far"])
+def test_exact_ties_take_the_lowest_index(name, ov, where):
+    # An exact tie (gap 0 in exact arithmetic) is never excused by the comparator: duplicated rows must
+    # give the lowest index at every layer, within a vocabulary tile ("near": copies 1-3 rows away, before
+    # and after the target) and across tiles ("far": about V/2 away, in another tile and another XCD's
+    # range). The streaming kernel sums each tile in its own chunk order, so across its tiles the
+    # reduction resolves such ties; the eager and the lazy path (every position walking) are both checked.
+    cfg = CONFIGS["llada_late"].with_(name="dup_" + name, masked_frac=None, sharp=("calibrated", 0.0, 3.0),
+                                      unstable_frac=0.3).with_(**ov)
+    w = make_workload(cfg, 60)
+    variant = rpd.projection_variant(cfg.K, cfg.B, cfg.L, cfg.d, cfg.V,
+                                     rpd.DTYPE_BF16 if cfg.dtype == "bf16" else rpd.DTYPE_F32,
+                                     max_masked=w.n_masked)
+    assert name.startswith(variant), (name, variant)
+    shifts = (1, 3, -2) if where == "near" else (cfg.V // 2 + 7, -(cfg.V // 2) - 5)
+    _duplicate_rows(w, shifts)
+    o = run_oracle(w, O.LLADA)
+    m = w.mask != 0
+    assert (o["layer_gap"][:, m] == 0.0).mean() > 0.9     # nearly every position's top is an exact tie
+    lazy = dataclasses.replace(O.LLADA, lazy=True, lazy_all=True)
+    for P in (O.LLADA,) + ((lazy,) if w.n_masked <= 100 else ()):   # the lazy oracle projects row by row
+        _check(w, P)     # an exact tie is never excused: any other index than the oracle's fails
+
+
+@pytest.mark.parametrize("name,ov", DUP_CASES, ids=[c[0] for c in DUP_CASES])
+def test_zero_hidden_rows_give_the_uniform_distribution(name, ov):
+    # Eq. 1 on z = 0: every logit exactly 0, p = 1/V, H = ln V, c = 1/V, and the argmax is index 0 (the
+    # lowest index among V exact ties) at every layer
+    cfg = CONFIGS["llada_late"].with_(name="zero_" + name, masked_frac=None).with_(**ov)
+    w = make_workload(cfg, 61)
+    w.hidden[:, w.mask != 0] = 0
+    g, o, rep = _check(w, O.LLADA)
+    m = w.mask != 0
+    V = cfg.V
+    assert (g["layer_argmax"][:, m] == 0).all() and (g["token"][m] == 0).all()
+    np.testing.assert_allclose(g["layer_entropy"][:, m], math.log(V), atol=2e-3)
+    np.testing.assert_allclose(g["layer_conf"][:, m], 1.0 / V, rtol=1e-3)
+    assert not (g["flags"][m] & rpd.FLAG_CANDIDATE).any()
+    assert (g["n_commit"] == (w.mask.sum(1) > 0)).all()     # the fallback alone commits
 
 
 def test_all_masked_and_single_layer():
@@ -462,6 +571,63 @@ def test_dream_full_size_sampled():
         g = run_gpu(w, P)
         _commit_property(g, w.mask, P)
     _sampled(w, P, g, 10, np.random.default_rng(3))
+
+
+# Whole full-size calls against the oracle at every masked position and layer (the fp64 projection of
+# 64-256 positions at the LLaDA-8B / Dream-7B shapes takes the host some seconds to a minute). The oracle's
+# per-layer statistics are computed once per workload and reused for every rule and budget.
+
+@pytest.mark.slow
+@pytest.mark.parametrize("cfgname,seed", [("llada_100", 2), ("llada_50", 102), ("llada_25", 202), ("llada_10", 302)])
+def test_llada_full_size_full_oracle(cfgname, seed, llada_wu):
+    w = make_workload(cfgname, seed, w_u=llada_wu)
+    for P in (O.strict(4, 0.5), O.strict(4, 1.0), O.strict(4, 2.0), O.LLADA):
+        note(f"  rule theta_s={P.theta_s} w={P.w} beta={P.beta}")
+        _check(w, P)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("cfgname,seed", [("dream_100", 3), ("dream_50", 103)])
+def test_dream_full_size_full_oracle(cfgname, seed):
+    w = make_workload(cfgname, seed)
+    for P in (O.strict(4, 1.0), O.DREAM):
+        note(f"  rule theta_s={P.theta_s} w={P.w} beta={P.beta}")
+        _check(w, P)
+
+
+class _Seq:
+    """One sequence of a batched workload, as a workload of its own (the
+    oracle treats sequences independently)."""
+
+    def __init__(self, w, b):
+        self.cfg = w.cfg.with_(name=f"{w.cfg.name}[{b}]", B=1)
+        self.seed = w.seed
+        self.w_u = w.w_u
+        self.hidden = w.hidden[:, b:b + 1]
+        self.mask = w.mask[b:b + 1]
+
+    @property
+    def n_masked(self):
+        return int(self.mask.sum())
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("cfgname,seed,seqs", [("llada_batched", 4, (0, 5)), ("llada_batched32", 204, (17,))])
+def test_batched_whole_sequences_full_oracle(cfgname, seed, seqs, llada_wu):
+    # the batch runs as one call (12,288 / 49,152 projected rows: the 256 x 256 tiles in per-XCD groups);
+    # whole sequences of it are compared with the oracle run on that sequence alone
+    w = make_workload(cfgname, seed, w_u=llada_wu)
+    P = O.strict(4, 1.0)
+    g = run_gpu(w, P)
+    K = w.cfg.K
+    for b in seqs:
+        sw = _Seq(w, b)
+        gs = {k: (v[:, b:b + 1] if v.ndim == 3 else v[b:b + 1]) for k, v in g.items() if k != "status"}
+        o = run_oracle(sw, P)
+        rep = compare(gs, o, sw.mask, P, w.cfg.d)
+        note(f"  sequence {b}: " + rep.summary()[:300])
+        assert rep.ok(), rep.summary()
+        assert sum(rep.excused.values()) <= max(2, 0.05 * sw.n_masked * (K + 3)), rep.summary()
 
 
 BAND_HEAVY = dict(sharp=("calibrated", 1.0, 2.2), unstable_frac=0.05)
