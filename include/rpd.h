@@ -250,6 +250,27 @@ rpd_status rpd_score_commit_timed(const rpd_problem* p, const rpd_params* q, con
                                   void* const* events, int32_t n_events);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * rpd_score_commit without a workspace argument. The workspace is a
+ * library-owned static device array of RPD_NOALLOC_SCRATCH_BYTES on each
+ * GPU the library runs on, held until the process ends; the call allocates
+ * nothing (no hipMalloc, no allocating library routine). Problems whose
+ * rpd_workspace_size exceeds RPD_NOALLOC_SCRATCH_BYTES are rejected with
+ * RPD_ERR_WORKSPACE_TOO_SMALL before anything is enqueued (at the LLaDA-8B
+ * vocabulary, up to about 8,400 projected rows: K * max_masked). Every call
+ * on one GPU shares that GPU's array: calls that overlap on one GPU (other
+ * streams, other threads) race and must be serialised by the caller. The
+ * array's prior contents never matter (every kernel writes what it reads).
+ * The first call on a device, with that device current, looks the array's
+ * address up (RPD_ERR_HIP if that fails). Otherwise exactly
+ * rpd_score_commit, including its validation and error reporting.
+ */
+#define RPD_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+rpd_status rpd_score_commit_noalloc(const rpd_problem* p, const rpd_params* q, const rpd_outputs* o,
+                                    void* stream);
+
+/*
  * Scoring and commitment from per-layer statistics that the caller already
  * has (Eq. 2-5 and Section 3.2), for callers whose logits come from
  * elsewhere. layer_argmax / layer_conf / layer_entropy are device [K][B][L]

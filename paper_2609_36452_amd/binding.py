@@ -116,6 +116,9 @@ def lib() -> ctypes.CDLL:
         L.rpd_score_commit_timed.argtypes = [ctypes.POINTER(RpdProblem), ctypes.POINTER(RpdParams),
                                              ctypes.POINTER(RpdOutputs), ctypes.c_void_p, ctypes.c_size_t,
                                              ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32]
+        L.rpd_score_commit_noalloc.restype = ctypes.c_int
+        L.rpd_score_commit_noalloc.argtypes = [ctypes.POINTER(RpdProblem), ctypes.POINTER(RpdParams),
+                                               ctypes.POINTER(RpdOutputs), ctypes.c_void_p]
         L.rpd_gate_commit.restype = ctypes.c_int
         L.rpd_gate_commit.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -293,6 +296,36 @@ def score_commit(hidden: torch.Tensor, w_u: torch.Tensor, mask: torch.Tensor, pa
     include/rpd.h), valid once the stream has run."""
     return ScoreCommit(hidden, w_u, mask, params, max_masked, layer_stats, norm_weight, norm_eps,
                        norm_final)(stream)
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20   # RPD_NOALLOC_SCRATCH_BYTES
+
+
+def score_commit_noalloc(hidden: torch.Tensor, w_u: torch.Tensor, mask: torch.Tensor, params: Params,
+                         max_masked: int | None = None, layer_stats: bool = False, stream=None,
+                         norm_weight: torch.Tensor | None = None, norm_eps: float = 1e-5, norm_final: bool = False,
+                         out: dict | None = None) -> dict:
+    """``rpd_score_commit_noalloc``: the commit step on the library's static
+    scratch array instead of a workspace (for callers that cannot allocate
+    device memory; calls that overlap on one GPU race). ``out``: output
+    tensors from a previous call or ``alloc_outputs`` (allocated here if
+    None). Returns the output tensors."""
+    K, B, L, d = hidden.shape
+    V = w_u.shape[0]
+    _check_dev("hidden", hidden, (K, B, L, d), (hidden.dtype,))
+    _check_dev("w_u", w_u, (V, d), (hidden.dtype,))
+    _check_dev("mask", mask, (B, L), (torch.uint8, torch.bool))
+    if norm_weight is not None:
+        _check_dev("norm_weight", norm_weight, (d,), (hidden.dtype,))
+    mm = -1 if max_masked is None else int(max_masked)
+    problem = make_problem(K, B, L, d, V, _dtype_code(hidden), hidden, w_u, mask.view(torch.uint8), mm,
+                           norm_weight, norm_eps, norm_final)
+    o = alloc_outputs(K, B, L, hidden.device, layer_stats) if out is None else out
+    q = params.to_c()
+    oc = _outputs_struct(o)
+    _check(lib().rpd_score_commit_noalloc(ctypes.byref(problem), ctypes.byref(q), ctypes.byref(oc),
+                                          _stream_handle(stream)))
+    return o
 
 
 def gate_commit(mask: torch.Tensor, layer_argmax: torch.Tensor, layer_conf: torch.Tensor,

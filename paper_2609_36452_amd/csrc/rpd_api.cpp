@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "rpd.h"
 #include "rpd_launch.h"
@@ -203,6 +204,38 @@ hipError_t run_lazy(rpd::Launch& a, int dtype, hipStream_t s, Mark& mark) {
 
 }  // namespace
 
+// The workspace of rpd_score_commit_noalloc: one static device array per
+// GPU, for callers that cannot allocate. In host code `scratch` names a
+// host-side stand-in, not device memory: only the address that
+// hipGetSymbolAddress returns for the current device is ever used.
+static __device__ __align__(256) unsigned char scratch[RPD_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};   // device address of `scratch` per device (looked up once)
+
+// the current device's address of `scratch`, looked up on its first use with that device current
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!ptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
 extern "C" {
 
 size_t rpd_workspace_size(const rpd_problem* p) {
@@ -342,6 +375,26 @@ rpd_status rpd_score_commit_timed(const rpd_problem* p, const rpd_params* q, con
                                   void* workspace, size_t workspace_bytes, void* stream, void* const* events,
                                   int32_t n_events) {
   return score_commit_impl(p, q, o, workspace, workspace_bytes, stream, events, n_events);
+}
+
+rpd_status rpd_score_commit_noalloc(const rpd_problem* p, const rpd_params* q, const rpd_outputs* o,
+                                    void* stream) {
+  g_err[0] = '\0';
+  if (!p) return fail(RPD_ERR_NULL_POINTER, "problem is NULL");
+  // the size first: a problem beyond the array is refused before any HIP call
+  const size_t need = rpd_workspace_size(p);
+  if (need > RPD_NOALLOC_SCRATCH_BYTES)
+    return fail(RPD_ERR_WORKSPACE_TOO_SMALL,
+                "the problem needs %zu workspace bytes; rpd_score_commit_noalloc has %zu (use rpd_score_commit with a "
+                "workspace of that size)", need, (size_t)RPD_NOALLOC_SCRATCH_BYTES);
+  // an invalid shape or dtype (need 0) is reported by the validation in score_commit_impl, which checks
+  // them before the workspace
+  void* ws = nullptr;
+  if (need > 0) {
+    const hipError_t e = scratch_address(&ws);
+    if (e != hipSuccess) return fail(RPD_ERR_HIP, "looking up the scratch array: %s", hipGetErrorString(e));
+  }
+  return score_commit_impl(p, q, o, ws, RPD_NOALLOC_SCRATCH_BYTES, stream, nullptr, 0);
 }
 
 rpd_status rpd_apply_commit(int32_t B, int32_t L, uint8_t* mask, int32_t* canvas, const uint8_t* commit,

@@ -153,6 +153,17 @@ def test_null_and_workspace_checks():
     assert _call(_prob(), _params(), _fake_outputs(), ws=256 + 16)[0] == 5
 
 
+def test_noalloc_refuses_problems_beyond_its_array_before_any_device_call():
+    # RPD_NOALLOC_SCRATCH_BYTES = 64 MiB; 32768 projected rows at the LLaDA-8B vocabulary need about 260 MB
+    p = _prob(B=8, L=1024, max_masked=-1)
+    need = int(rpd.lib().rpd_workspace_size(ctypes.byref(p)))
+    assert need > rpd.NOALLOC_SCRATCH_BYTES
+    s = rpd.lib().rpd_score_commit_noalloc(ctypes.byref(p), ctypes.byref(_params()), ctypes.byref(_fake_outputs()),
+                                           None)
+    assert s == 4 and "workspace" in rpd.last_error()
+    assert rpd.lib().rpd_score_commit_noalloc(None, ctypes.byref(_params()), ctypes.byref(_fake_outputs()), None) == 1
+
+
 def test_gate_validation():
     L = rpd.lib()
     q = _params()
