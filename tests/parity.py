@@ -145,18 +145,25 @@ def compare(g: dict, o: dict, mask: np.ndarray, P, d: int, layer: bool = True) -
             gh, oh = g["layer_entropy"][l], o["layer_entropy"][l]
             for b, i in zip(*np.nonzero(m)):
                 rep.checked["layer"] += 1
-                if lazy_excuse[b, i] and l < K - 1:
-                    rep.excused["lazy_layer"] += 1
-                    continue
+                issues = []
                 if np.isnan(oh[b, i]):
                     if not (np.isnan(gh[b, i]) and np.isnan(gc[b, i])):
-                        rep.bad(f"NaN row not NaN on GPU at l={l} b={b} i={i}")
+                        issues.append(f"NaN row not NaN on GPU at l={l} b={b} i={i}")
+                else:
+                    if not abs(gh[b, i] - oh[b, i]) <= ENTROPY_TOL:
+                        issues.append(f"entropy l={l} b={b} i={i}: gpu {gh[b, i]:.6g} oracle {oh[b, i]:.6g}")
+                    if not abs(gc[b, i] - oc[b, i]) <= CONF_TOL:
+                        issues.append(f"conf l={l} b={b} i={i}: gpu {gc[b, i]:.6g} oracle {oc[b, i]:.6g}")
+                argmax_differs = gy[b, i] != oy[b, i]
+                if not issues and not argmax_differs:
                     continue
-                if abs(gh[b, i] - oh[b, i]) > ENTROPY_TOL:
-                    rep.bad(f"entropy l={l} b={b} i={i}: gpu {gh[b, i]:.6g} oracle {oh[b, i]:.6g}")
-                if abs(gc[b, i] - oc[b, i]) > CONF_TOL:
-                    rep.bad(f"conf l={l} b={b} i={i}: gpu {gc[b, i]:.6g} oracle {oc[b, i]:.6g}")
-                if gy[b, i] != oy[b, i]:
+                if lazy_excuse[b, i] and l < K - 1:
+                    # which intermediate layers a lazy walk reaches depends on a near-tie here
+                    rep.excused["lazy_layer"] += 1
+                    continue
+                for msg in issues:
+                    rep.bad(msg)
+                if argmax_differs:
                     if tie[l, b, i]:
                         rep.excused["argmax_tie"] += 1
                     else:
@@ -173,7 +180,7 @@ def compare(g: dict, o: dict, mask: np.ndarray, P, d: int, layer: bool = True) -
                 rep.bad(f"NaN position b={b} i={i} became a candidate")
             continue
         for name, tol in (("entropy", ENTROPY_TOL), ("confidence", CONF_TOL)):
-            if abs(g[name][b, i] - o[name][b, i]) > tol:
+            if not abs(g[name][b, i] - o[name][b, i]) <= tol:     # a NaN on the GPU side fails too
                 rep.bad(f"{name} b={b} i={i}: gpu {g[name][b, i]:.6g} oracle {o[name][b, i]:.6g}")
         if g["token"][b, i] != o["token"][b, i]:
             if tie_final[b, i]:

@@ -63,7 +63,8 @@ def _clear(o, d):
 
 
 PLANTS = ["token", "layer_argmax", "entropy", "confidence", "layer_entropy", "layer_conf", "persistence",
-          "drop", "candidate_flag", "commit", "n_commit", "upstream_entropy", "sentinel", "committed_bit"]
+          "drop", "candidate_flag", "commit", "n_commit", "upstream_entropy", "sentinel", "committed_bit",
+          "nan_entropy", "nan_layer_conf"]
 
 
 @pytest.mark.parametrize("what", PLANTS)
@@ -103,6 +104,10 @@ def test_rejects_planted_mistake(case, what):
         g["token"][bb, ii] = 3
     elif what == "committed_bit":
         g["flags"][b, i] ^= 8
+    elif what == "nan_entropy":
+        g["entropy"][b, i] = np.nan
+    elif what == "nan_layer_conf":
+        g["layer_conf"][0, b, i] = np.nan
     rep = _run(w, P, o, g)
     assert not rep.ok(), f"{what} planted at {(b, i)} was accepted: {rep.summary()}"
 
