@@ -99,6 +99,18 @@ def copy_probe(torch) -> float:
     return gbs
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (for the CPU baseline's context)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def blas_threads() -> int:
     try:
         from threadpoolctl import threadpool_info
@@ -130,8 +142,135 @@ def cpu_baseline(w, P, budget_s: float) -> dict:
         reps += 1
     n = len(pos_all)
     return {"value": n * reps / t, "unit": "positions/s", "cores": blas_threads(), "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": f"{reps} whole call(s) of the step ({n} masked positions x {w.cfg.K} layers, "
                       f"V={w.cfg.V}, d={w.cfg.d}) in float64, {t:.1f} s"}
+
+
+def cpu_baseline_sampled(w, P, n_sample: int) -> dict:
+    """The fp64 oracle, as it is, on a bounded sample of a large workload: the
+    whole step on a canvas holding only the first n_sample masked positions
+    of sequence 0 (the oracle's cost is linear in the masked positions it
+    projects, so positions/s carries over to the whole batch)."""
+    import numpy as np
+    import oracle as O
+    idx = np.nonzero(w.mask[0])[0][:n_sample]
+    sub = np.zeros_like(w.mask)
+    sub[0, idx] = 1
+    t0 = time.perf_counter()
+    O.score_commit(w.hidden, w.w_u, sub, w.cfg.dtype, P)
+    t = time.perf_counter() - t0
+    return {"value": len(idx) / t, "unit": "positions/s", "cores": blas_threads(), "kind": "oracle",
+            "cpu_model": cpu_model(),
+            "sample": f"one call of the step on the first {len(idx)} masked positions of sequence 0 only "
+                      f"({len(idx)} of {w.n_masked} positions x {w.cfg.K} layers, V={w.cfg.V}, d={w.cfg.d}) in "
+                      f"float64, {t:.1f} s; the oracle's cost is linear in the positions it projects"}
+
+
+def time_calls(call, steps: int, warmup: int, event_every: int, flush=None):
+    """Warm-up calls, then `steps` timed calls bracketed by events on the
+    current stream (torch's, which the library launches on). Every
+    `event_every`-th call also records events around the whole call and around
+    the projection kernel (rpd_score_commit_timed). Returns (ms over all
+    steps, projection ms per sampled call, call ms per sampled call); with a
+    flush the steps' time is the sum of the sampled (every) calls."""
+    import torch
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    E = 1 if flush is not None else max(1, event_every)
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    nev = (steps + E - 1) // E
+    proj_a, proj_b, call_a, call_b = ([ev() for _ in range(nev)] for _ in range(4))
+    start, end = ev(), ev()
+    for e in proj_a + proj_b + call_a + call_b:       # torch creates the HIP event at its first record
+        e.record()
+    torch.cuda.synchronize()
+    assert all(e.cuda_event for e in proj_a + proj_b + call_a + call_b)
+    start.record()
+    for k in range(steps):
+        if flush is not None:
+            flush.fill_(k & 255)          # evicts W_U, hidden rows and outputs from the 256 MB cache
+        if k % E == 0:
+            j = k // E
+            call(events=[call_a[j], proj_a[j], proj_b[j], None, call_b[j]])
+        else:
+            call()
+    end.record()
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(end)
+    call_ms = [a.elapsed_time(b) for a, b in zip(call_a, call_b)]
+    if flush is not None:    # the flushes are in the loop: time the calls alone
+        ms_total = float(sum(call_ms))
+    proj_ms = [a.elapsed_time(b) for a, b in zip(proj_a, proj_b)]
+    return ms_total, proj_ms, call_ms
+
+
+def roofline_entry(cfg, R: int, proj_ms_avg: float, call_ms_avg: float, variant: str) -> dict:
+    """Roofline of the projection kernel (algorithmic bytes or flops per launch
+    over its event-timed average) and of the whole call."""
+    bytes_alg, flops_alg = proj_cost(cfg, R)
+    t_bound = max(bytes_alg / (HBM_PEAK_GBS * 1e9), flops_alg / (MFMA_BF16_PEAK_TFLOPS * 1e12))
+    if R < RIDGE_ROWS:
+        achieved = bytes_alg / (proj_ms_avg / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    else:
+        achieved = flops_alg / (proj_ms_avg / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4)}
+    roof["traffic"] = read_traffic(variant, cfg.name)
+    roof["kernel"] = f"{VARIANT_KERNEL[variant]} ({variant})"
+    roof["kernel_us"] = round(proj_ms_avg * 1e3, 2)
+    roof["call_frac"] = round(t_bound / (call_ms_avg / 1e3), 4)
+    roof["alg_bytes_per_launch"] = bytes_alg
+    roof["alg_flops_per_launch"] = flops_alg
+    return roof
+
+
+def bench_mfma_regime(args, torch, rpd) -> dict:
+    """The compute-bound regime beside the headline: the batched LLaDA-8B
+    shape (8 sequences x 512 positions, 75% masked: 12,288 projected rows),
+    timed like the headline (events around every call and its projection)."""
+    import numpy as np
+    from paper_2609_36452_amd.workload import CONFIGS, make_workload
+    cfg = CONFIGS[args.mfma_config]
+    log(f"mfma regime: drawing workload {cfg.name} seed {args.seed}")
+    w = make_workload(cfg, args.seed)
+    P = rpd.Params.strict(cfg.K, args.beta)
+    dev = torch.device("cuda:0")
+    hidden = torch.from_numpy(w.hidden).view(torch.bfloat16).to(dev)
+    w_u = torch.from_numpy(w.w_u).view(torch.bfloat16).to(dev)
+    mask = torch.from_numpy(w.mask).to(dev)
+    call = rpd.ScoreCommit(hidden, w_u, mask, P, max_masked=w.n_masked)
+    variant = rpd.projection_variant(cfg.K, cfg.B, cfg.L, cfg.d, cfg.V, hidden.dtype, max_masked=w.n_masked)
+    K, W = args.mfma_steps, args.mfma_warmup
+    log(f"  variant {variant}; warmup {W}, timing {K} calls")
+    ms_total, proj_ms, call_ms = time_calls(call, K, W, 1)
+    n, R = w.n_masked, w.n_masked * cfg.K
+    ms_step = ms_total / K
+    proj_avg, call_avg = float(np.mean(proj_ms)), float(np.mean(call_ms))
+    log(f"  {ms_step * 1e3:.1f} us/step, projection {proj_avg * 1e3:.1f} us")
+    pct = lambda xs: {f"p{q}": round(float(np.percentile(xs, q)) * 1e3, 2) for q in (10, 50, 90)}  # noqa: E731
+    out = {
+        "workload": f"{cfg.name}: d={cfg.d} V={cfg.V} B={cfg.B} L={cfg.L} K={cfg.K} masked={n} ({R} projected "
+                    f"rows), rule=strict beta={P.beta}",
+        "value": round(n * K / (ms_total / 1e3), 1),
+        "unit": "positions/s",
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(ms_step, 5),
+        "iterations_per_s": round(1e3 / ms_step, 2),
+        "call_us_sampled": pct(call_ms),
+        "projection_us_sampled": pct(proj_ms),
+        "roofline": roofline_entry(cfg, R, proj_avg, call_avg, variant),
+    }
+    del call, hidden, mask
+    if not args.no_cpu_baseline:
+        import oracle as O
+        log("  cpu baseline (oracle, sampled)")
+        out["cpu_baseline"] = cpu_baseline_sampled(w, O.Params(**P.__dict__), args.mfma_cpu_positions)
+    return out
 
 
 def proj_cost(cfg, rows: int):
@@ -305,6 +444,13 @@ def main() -> int:
     ap.add_argument("--cold", action="store_true",
                     help="flush the last-level cache between calls with a 512 MB write (not timed: every call "
                          "carries events and the value comes from the per-call times)")
+    ap.add_argument("--mfma-config", default="llada_batched",
+                    help="the compute-bound workload timed beside the headline in the same line (mfma_regime); "
+                         "empty to skip")
+    ap.add_argument("--mfma-steps", type=int, default=20)
+    ap.add_argument("--mfma-warmup", type=int, default=5)
+    ap.add_argument("--mfma-cpu-positions", type=int, default=384,
+                    help="masked positions of the oracle's sample for the mfma_regime CPU baseline")
     ap.add_argument("--event-every", type=int, default=4,
                     help="record the projection's HIP events on every N-th timed call (each event record "
                          "costs the stream a few microseconds)")
@@ -361,70 +507,22 @@ def main() -> int:
     variant = rpd.projection_variant(cfg.K, cfg.B, cfg.L, cfg.d, cfg.V, hidden.dtype, max_masked=w.n_masked)
     log(f"projection variant {variant}")
     torch.cuda.synchronize()
-    log(f"warmup {args.warmup}")
-    for _ in range(args.warmup):
-        call()
-    torch.cuda.synchronize()
-
     K = args.steps
-    E = 1 if args.cold else max(1, args.event_every)
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev) if args.cold else None
-    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
-    proj_a = [ev() for _ in range((K + E - 1) // E)]
-    proj_b = [ev() for _ in range((K + E - 1) // E)]
-    call_a = [ev() for _ in range((K + E - 1) // E)]
-    call_b = [ev() for _ in range((K + E - 1) // E)]
-    start, end = ev(), ev()
-    for e in proj_a + proj_b + call_a + call_b:       # torch creates the HIP event at its first record
-        e.record()
-    torch.cuda.synchronize()
-    assert all(e.cuda_event for e in proj_a + proj_b + call_a + call_b)
-    log(f"timing {K} steps")
-    torch.cuda.synchronize()
+    log(f"warmup {args.warmup}, timing {K} steps")
     t_wall0 = time.perf_counter()
-    start.record()
-    for k in range(K):
-        if flush is not None:
-            flush.fill_(k & 255)          # evicts W_U, hidden rows and outputs from the 256 MB cache
-        if k % E == 0:
-            j = k // E
-            call(events=[call_a[j], proj_a[j], proj_b[j], None, call_b[j]])
-        else:
-            call()
-    end.record()
-    torch.cuda.synchronize()
+    ms_total, proj_ms, call_ms = time_calls(call, K, args.warmup, args.event_every, flush)
     t_wall = time.perf_counter() - t_wall0
-    ms_total = start.elapsed_time(end)
     ms_step = ms_total / K
-    if flush is not None:    # the flushes are in the loop: time the calls alone
-        ms_total = float(sum(a.elapsed_time(b) for a, b in zip(call_a, call_b)))
-        ms_step = ms_total / K
-    proj_ms = [a.elapsed_time(b) for a, b in zip(proj_a, proj_b)]
     proj_avg = float(np.mean(proj_ms))
-    call_ms = [a.elapsed_time(b) for a, b in zip(call_a, call_b)]
     pct = lambda xs: {f"p{q}": round(float(np.percentile(xs, q)) * 1e3, 2) for q in (10, 50, 90)}  # noqa: E731
     n = w.n_masked
     R = n * cfg.K
     value = n * K / (ms_total / 1e3)
     log(f"  {ms_step * 1e3:.1f} us/step, projection {proj_avg * 1e3:.1f} us (median "
         f"{np.median(proj_ms) * 1e3:.1f}), wall {t_wall:.3f} s")
-
-    bytes_alg = cfg.V * cfg.d * (2 if cfg.dtype == "bf16" else 4) + R * cfg.d * (2 if cfg.dtype == "bf16" else 4)
-    flops_alg = 2.0 * R * cfg.V * cfg.d
-    if R < RIDGE_ROWS:
-        achieved = bytes_alg / (proj_avg / 1e3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4)}
-    else:
-        achieved = flops_alg / (proj_avg / 1e3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4)}
-    roof["traffic"] = read_traffic(variant, cfg.name)
-    roof["kernel"] = f"{VARIANT_KERNEL[variant]} ({variant})"
-    roof["kernel_us"] = round(proj_avg * 1e3, 2)
+    roof = roofline_entry(cfg, R, proj_avg, float(np.mean(call_ms)), variant)
     roof["timed_launches"] = len(proj_ms)
-    roof["alg_bytes_per_launch"] = bytes_alg
-    roof["alg_flops_per_launch"] = flops_alg
 
     out = {
         "metric": METRIC,
@@ -454,6 +552,7 @@ def main() -> int:
         "projection_us_sampled": pct(proj_ms),
         "roofline": roof,
     }
+    del call
     if not args.no_copy_probe:
         out["copy_probe_gbs"] = round(copy_probe(torch), 1)
     if not args.no_cpu_baseline and not args.norm:
@@ -461,6 +560,8 @@ def main() -> int:
         OP = O.Params(**P.__dict__)
         log("cpu baseline (oracle)")
         out["cpu_baseline"] = cpu_baseline(w, OP, args.cpu_budget)
+    if args.mfma_config and args.mfma_config != cfg.name and not args.norm and not args.lazy and not args.cold:
+        out["mfma_regime"] = bench_mfma_regime(args, torch, rpd)
     print(json.dumps(out), flush=True)
     return 0
 
