@@ -25,6 +25,7 @@ FLAG_COMMITTED = 8
 FLAG_FALLBACK = 16
 
 DEVICE_STATUS_MASKED_OVERFLOW = 1
+ABI_VERSION = 3   # RPD_ABI_VERSION: the layouts and entry points this binding marshals for
 PARAM_LAZY = 1
 PARAM_LAZY_ALL = 2
 
@@ -135,6 +136,9 @@ def lib() -> ctypes.CDLL:
         L.rpd_projection_variant.argtypes = [ctypes.POINTER(RpdProblem)]
         L.rpd_abi_version.restype = ctypes.c_int32
         L.rpd_abi_version.argtypes = []
+        if L.rpd_abi_version() != ABI_VERSION:
+            raise RuntimeError(f"{_LIB_PATH} has ABI version {L.rpd_abi_version()}, this binding needs "
+                               f"{ABI_VERSION}: rebuild the library")
         _lib = L
     return _lib
 

@@ -40,7 +40,9 @@ def test_struct_layouts():
 
 
 def test_version_and_status_strings():
-    assert rpd.abi_version() == 3
+    assert rpd.abi_version() == 3 == rpd.ABI_VERSION
+    hdr = open(os.path.join(ROOT, "include", "rpd.h")).read()
+    assert "#define RPD_ABI_VERSION 3\n" in hdr
     assert rpd.status_string(0) == "ok"
     assert rpd.status_string(4) == "workspace too small"
 
