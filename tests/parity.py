@@ -146,7 +146,9 @@ def compare(g: dict, o: dict, mask: np.ndarray, P, d: int, layer: bool = True) -
             for b, i in zip(*np.nonzero(m)):
                 rep.checked["layer"] += 1
                 issues = []
-                if np.isnan(oh[b, i]):
+                nan_row = bool(np.isnan(oh[b, i]))
+                if nan_row:
+                    # a distribution with undefined entries: both statistics NaN, no argmax to compare
                     if not (np.isnan(gh[b, i]) and np.isnan(gc[b, i])):
                         issues.append(f"NaN row not NaN on GPU at l={l} b={b} i={i}")
                 else:
@@ -154,7 +156,7 @@ def compare(g: dict, o: dict, mask: np.ndarray, P, d: int, layer: bool = True) -
                         issues.append(f"entropy l={l} b={b} i={i}: gpu {gh[b, i]:.6g} oracle {oh[b, i]:.6g}")
                     if not abs(gc[b, i] - oc[b, i]) <= CONF_TOL:
                         issues.append(f"conf l={l} b={b} i={i}: gpu {gc[b, i]:.6g} oracle {oc[b, i]:.6g}")
-                argmax_differs = gy[b, i] != oy[b, i]
+                argmax_differs = (not nan_row) and gy[b, i] != oy[b, i]
                 if not issues and not argmax_differs:
                     continue
                 if lazy_excuse[b, i] and l < K - 1:

@@ -206,6 +206,34 @@ def test_intermediate_tie_does_not_excuse_a_token_mismatch():
     assert not compare(g, o, mask, P, 8).ok()
 
 
+def _nan_row_case():
+    # the tie case's position with one NaN hidden element at every layer: every logit is NaN
+    hidden, w_u, mask = _two_row_case(0.5)
+    hidden[:, 0, 0, 3] = np.nan
+    P = O.Params(theta_s=1.0, w=1.0)
+    return O.score_commit(hidden, w_u, mask, "f32", P), mask, P
+
+
+def test_nan_row_has_no_argmax_to_compare():
+    o, mask, P = _nan_row_case()
+    assert np.isnan(o["layer_entropy"][:, 0, 0]).all() and np.isnan(o["entropy"][0, 0])
+    g = as_gpu_outputs(o)
+    g["layer_argmax"][:, 0, 0] = -1       # the GPU finds no ordered maximum in such a row
+    g["token"][0, 0] = -1
+    rep = compare(g, o, mask, P, 8)
+    assert rep.ok(), rep.summary()
+
+
+def test_nan_row_must_stay_nan_and_not_a_candidate():
+    o, mask, P = _nan_row_case()
+    g = as_gpu_outputs(o)
+    g["layer_entropy"][0, 0, 0] = 0.5
+    assert not compare(g, o, mask, P, 8).ok()
+    g = as_gpu_outputs(o)
+    g["flags"][0, 0] |= F_CAND
+    assert not compare(g, o, mask, P, 8).ok()
+
+
 # ------------------------------------------------- near-tie diagnostics pin --
 
 def test_gap_and_absbound_against_brute_force():
