@@ -52,7 +52,18 @@ namespace {
 // cycles in the main loop, 3.5% less time (the chip then runs at its power
 // limit and lowers the clock); the epilogue without validity selects on full
 // tiles: 38% fewer epilogue cycles; buffer loads for W_U, then for the hidden
-// rows: 4% and 6% fewer main-loop cycles (9.5 ms at 12288 rows on one GPU).
+// rows: 4% and 6% fewer main-loop cycles (9.5 ms at 12288 rows on one GPU);
+// the epilogue's sums in base-2 units from one fma per logit and 3-input
+// maxima: 0.2-1.6% less time from 192 to 12288 rows (interleaved A/B), the
+// 256-row form's spills down from 19 VGPRs to 3. Per tile at 12288 rows
+// (shader clock read at the phase boundaries): 9.5k cycles until the first
+// chunk has landed, 136.4k in the main loop (131k of MFMA issue), 15.4k in
+// the epilogue, 2k between tiles; the clock, read against the fixed 100 MHz
+// counter, was 1.61 GHz there and 1.2-1.55 GHz at 256-1024 rows in the same
+// run, so the chip's power limit, not the schedule, sets most of the time.
+// A persistent form (one workgroup per CU looping over its tiles, the next
+// tile's W_U chunks loaded during the epilogue) spilled 110-140 VGPRs per
+// tile at 256 rows and measured 9-15% slower.
 namespace big {
 constexpr int TV = kBigTileVocab, KC = 64;
 }  // namespace big
@@ -311,21 +322,25 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
   // vocabulary rows 128*wv + 32*mv + 8*(q >> 2) + 4*(lane >> 5) + (q & 3)
   if (ve - vb == TV) {
     // A full vocabulary tile: no entry to exclude. Each projected row's 64
-    // logits in this lane take one max pass over the raw accumulators (the
-    // scale is positive and rounding is monotone, so the scaled maximum is
-    // the maximum of the scaled logits), then one pass for the sums. Slot e
-    // holds acc[e >> 4][nb][e & 15]; the lowest slot equal to the maximum is
-    // the lane's argmax (slots increase with the vocabulary index).
+    // raw accumulators in this lane take one max pass (3-input maxima); the
+    // scale is positive, so the lowest slot holding the raw maximum is the
+    // argmax of the scaled logits (slots increase with the vocabulary
+    // index). The sums are taken in base-2 units: t = (z - m) log2(e) in one
+    // fma from the raw accumulator, e^(z-m) = 2^t, and T = ln(2) sum 2^t t.
+    const float s2 = scale * 1.44269504088896340736f;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      float mr[4];
+      float mraw = acc[0][nb][0];
 #pragma unroll
-      for (int mv = 0; mv < 4; ++mv) {
-        mr[mv] = acc[mv][nb][0];
+      for (int mv = 0; mv < 4; ++mv)
 #pragma unroll
-        for (int q = 1; q < 16; ++q) mr[mv] = fmaxf(mr[mv], acc[mv][nb][q]);
-      }
-      const float m = fmaxf(fmaxf(mr[0], mr[1]), fmaxf(mr[2], mr[3])) * scale;
+        for (int q = (mv == 0 ? 1 : 0); q < 16; q += 2) {
+          if (q + 1 < 16)
+            mraw = __builtin_fmaxf(mraw, __builtin_fmaxf(acc[mv][nb][q], acc[mv][nb][q + 1]));
+          else
+            mraw = __builtin_fmaxf(mraw, acc[mv][nb][q]);
+        }
+      const float m2 = mraw * s2;
       int slot = 64;
       float Sp[4], Tp[4];
 #pragma unroll
@@ -334,19 +349,19 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
         Tp[mv] = 0.f;
 #pragma unroll
         for (int q = 15; q >= 0; --q) {
-          const float z = acc[mv][nb][q] * scale;
-          slot = z == m ? 16 * mv + q : slot;
-          const float dz = z - m;
-          const float ex = __expf(dz);
+          const float a = acc[mv][nb][q];
+          slot = a == mraw ? 16 * mv + q : slot;
+          const float t = __builtin_fmaf(a, s2, -m2);
+          const float ex = __builtin_amdgcn_exp2f(t);
           Sp[mv] += ex;
-          Tp[mv] = fmaf(ex, dz, Tp[mv]);
+          Tp[mv] = __builtin_fmaf(ex, t, Tp[mv]);
         }
       }
       Soft sst;
-      sst.m = m;
+      sst.m = mraw * scale;
       sst.S = (Sp[0] + Sp[1]) + (Sp[2] + Sp[3]);
-      sst.T = (Tp[0] + Tp[1]) + (Tp[2] + Tp[3]);
-      sst.idx = (slot == 64 || m == -INFINITY)
+      sst.T = ((Tp[0] + Tp[1]) + (Tp[2] + Tp[3])) * 0.69314718055994530942f;
+      sst.idx = (slot == 64 || mraw == -INFINITY)
                     ? INT_MAX
                     : vb + 128 * wv + 32 * (slot >> 4) + 8 * ((slot >> 2) & 3) + 4 * (lane >> 5) + (slot & 3);
       sst = soft_merge(sst, soft_shfl_xor(sst, 32));
