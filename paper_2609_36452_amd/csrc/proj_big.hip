@@ -242,16 +242,23 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
     __builtin_amdgcn_sched_barrier(0);                                                                    \
   } while (0)
 
-  // Chunks past the end repeat the last one (loaded, never multiplied). Every
-  // tile takes the chunks in plain order, so every vocabulary row's products
-  // are summed the same way and equal W_U rows give bit-identical logits (an
-  // exact tie goes to the lowest index). Starting each tile at its own chunk,
-  // as the streaming kernel does against HBM channel crowding, measured
-  // neutral here with a single row tile and 7-8% slower from 1024 rows up,
-  // where the workgroups of one row tile share its hidden rows through L2
-  // only while they read the same chunk.
+  // Chunks past the end repeat the last one (loaded, never multiplied). With a
+  // single row tile (NT) the workgroups of XCD x (workgroup id mod 8) take
+  // the full chunks in the order r, r+1, .., nchf-1, 0, .., r-1 with
+  // r = x*nchf/8: the requests in flight on the eight XCDs then read eight
+  // different columns of W_U (in plain order they all read one column and
+  // crowd onto a few HBM channels on some boxes: 226 against 176 us at 104
+  // rows, 253 against 203 at 192), while the workgroups of one XCD still
+  // read the same hidden-row chunk at a time through its L2 (a rotation by
+  // vocabulary tile cost 2-8% at 104-256 rows on boxes without the
+  // crowding). Equal rows within a tile are summed in one order and tie
+  // exactly; across tiles the reduction settles a near-tie in float64
+  // (reduce_device.h). With several row tiles the plain order stays: the
+  // workgroups of one row tile share its hidden rows through L2 only while
+  // they read the same chunk (rotated, 7-8% slower from 1024 rows up).
   const int nchf = d / KC;
-#define RPD_PCHUNK(c) (c)
+  const int rot = NT && nchf > 0 ? (int)(((long long)(blockIdx.x & 7) * nchf) / 8) : 0;
+#define RPD_PCHUNK(c) ((c) + rot >= nchf ? (c) + rot - nchf : (c) + rot)
   if (nchf > 0) {
     RPD_ALOAD(0, 0);
     RPD_BLOAD(0, 0);

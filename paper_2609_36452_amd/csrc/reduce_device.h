@@ -12,8 +12,9 @@ namespace {
 // ------------------------------------------------------ exact argmax ties --
 //
 // The streaming projection takes each vocabulary tile's k-chunks in its own
-// rotated order (against HBM channel crowding), so two equal W_U rows in
-// different tiles can round to different fp32 logits, and the cross-tile
+// rotated order, and the MFMA tile with a single row tile one order per XCD
+// (both against HBM channel crowding), so two equal W_U rows in different
+// tiles can round to different fp32 logits, and the cross-tile
 // merge alone would then not give the lowest index of an exact tie. After
 // the merge, every tile whose best row has a lower index than the winner y
 // and a maximum below it by at most the accumulation-rounding bound
@@ -36,21 +37,37 @@ struct TieArgs {
 // 8-element pieces l, l+64, ... in turn, then a fixed xor butterfly (each
 // step adds two equal-shaped partial sums, and addition commutes, so every
 // lane ends with the same value). Products of bf16 values are exact in
-// float64.
+// float64. A lane issues the loads of eight pieces before it uses any (a
+// single memory round trip at d <= 4096; one per piece in turn cost the
+// call 5-6 us whenever a row was checked).
 __device__ __forceinline__ void canon_dot_bf16(const uint16_t* __restrict__ w, const uint16_t* __restrict__ x,
                                                int d, int lane, double& z, double& a) {
   double zs = 0.0, as = 0.0;
-  for (int pc = lane; 8 * pc < d; pc += 64) {
-    const u32x4 wv = *reinterpret_cast<const u32x4*>(w + 8 * pc);
-    const u32x4 xv = *reinterpret_cast<const u32x4*>(x + 8 * pc);
+  for (int p0 = lane; 8 * p0 < d; p0 += 64 * 8) {
+    u32x4 wv[8], xv[8];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const double p0 = (double)__uint_as_float(wv[e] << 16) * (double)__uint_as_float(xv[e] << 16);
-      const double p1 = (double)__uint_as_float(wv[e] & 0xffff0000u) * (double)__uint_as_float(xv[e] & 0xffff0000u);
-      zs += p0;
-      as += fabs(p0);
-      zs += p1;
-      as += fabs(p1);
+    for (int u = 0; u < 8; ++u) {
+      const int pc = p0 + 64 * u;
+      wv[u] = u32x4{0u, 0u, 0u, 0u};
+      xv[u] = u32x4{0u, 0u, 0u, 0u};
+      if (8 * pc < d) {
+        wv[u] = *reinterpret_cast<const u32x4*>(w + 8 * pc);
+        xv[u] = *reinterpret_cast<const u32x4*>(x + 8 * pc);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (8 * (p0 + 64 * u) >= d) break;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double p0_ = (double)__uint_as_float(wv[u][e] << 16) * (double)__uint_as_float(xv[u][e] << 16);
+        const double p1_ =
+            (double)__uint_as_float(wv[u][e] & 0xffff0000u) * (double)__uint_as_float(xv[u][e] & 0xffff0000u);
+        zs += p0_;
+        as += fabs(p0_);
+        zs += p1_;
+        as += fabs(p1_);
+      }
     }
   }
 #pragma unroll
@@ -67,10 +84,13 @@ __device__ __forceinline__ bool tie_candidate(const Soft& q, const Soft& s, floa
 }
 
 // The tie resolution a reduction needs after a projection run with plan pl:
-// only the streaming variants take rotated chunk orders (with two or more
-// full 64-wide chunks).
+// needed where vocabulary tiles take their full 64-wide chunks in rotated
+// orders (two or more of them).
 inline TieArgs tie_args(const Launch& a, const ProjPlan& pl) {
-  const bool rotated = (pl.variant == PROJ_BF16_S32 || pl.variant == PROJ_BF16_S64) && a.d / 64 >= 2;
+  // the streaming kernels, and the MFMA tiles with a single row tile
+  const bool big = pl.variant == PROJ_BF16_BIG || pl.variant == PROJ_BF16_BIG192 || pl.variant == PROJ_BF16_BIG128;
+  const bool rotated = (pl.variant == PROJ_BF16_S32 || pl.variant == PROJ_BF16_S64 || (big && pl.nrt == 1)) &&
+                       a.d / 64 >= 2;
   return TieArgs{rotated ? static_cast<const uint16_t*>(a.w_u) : nullptr, a.d, a.logit_scale};
 }
 
