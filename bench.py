@@ -273,6 +273,58 @@ def bench_mfma_regime(args, torch, rpd) -> dict:
     return out
 
 
+def bench_library_gemm(args, torch, rpd) -> int:
+    """Calibration, not the benchmark: the vendor library's plain bf16 GEMM
+    (torch.mm, hipBLASLt) of the same masked rows against the same W_U, timed
+    alternately with the projection of the commit step on the same data. The
+    GEMM writes the R x V product and has no softmax; the projection writes
+    per-tile softmax states only. One JSON line per workload."""
+    import numpy as np
+    from paper_2609_36452_amd.workload import CONFIGS, make_workload
+    dev = torch.device("cuda:0")
+    for name in args.library_gemm.split(","):
+        cfg = CONFIGS[name]
+        log(f"library gemm: drawing workload {cfg.name} seed {args.seed}")
+        w = make_workload(cfg, args.seed)
+        hidden = torch.from_numpy(w.hidden).view(torch.bfloat16).to(dev)
+        w_u = torch.from_numpy(w.w_u).view(torch.bfloat16).to(dev)
+        mask = torch.from_numpy(w.mask).to(dev)
+        n, R = w.n_masked, w.n_masked * cfg.K
+        pos = mask.reshape(-1).nonzero().reshape(-1)
+        # the projected rows in the commit step's order: position-major, layer-minor
+        x = hidden.reshape(cfg.K, -1, cfg.d)[:, pos].permute(1, 0, 2).reshape(R, cfg.d).contiguous()
+        prod = torch.empty(R, cfg.V, dtype=torch.bfloat16, device=dev)
+        call = rpd.ScoreCommit(hidden, w_u, mask, rpd.Params.strict(cfg.K, args.beta), max_masked=n)
+        N = args.steps
+        for _ in range(args.warmup):
+            call()
+            torch.mm(x, w_u.t(), out=prod)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(N)]
+        for e in ev:   # the binding records through HIP: each event needs its handle first
+            for x_ in e:
+                x_.record()
+        torch.cuda.synchronize()
+        for e in ev:
+            call(events=[e[0], e[1], e[2], None, e[3]])
+            e[4].record()
+            torch.mm(x, w_u.t(), out=prod)
+            e[5].record()
+        torch.cuda.synchronize()
+        t_proj = float(np.median([e[1].elapsed_time(e[2]) for e in ev])) * 1e3
+        t_lib = float(np.median([e[4].elapsed_time(e[5]) for e in ev])) * 1e3
+        fl = 2.0 * R * cfg.V * cfg.d
+        print(json.dumps({
+            "workload": cfg.name, "projected_rows": R, "d": cfg.d, "V": cfg.V, "calls": N,
+            "projection_us_median": round(t_proj, 1), "library_gemm_us_median": round(t_lib, 1),
+            "projection_tflops": round(fl / t_proj / 1e6, 1), "library_gemm_tflops": round(fl / t_lib / 1e6, 1),
+            "projection_over_library": round(t_proj / t_lib, 4),
+            "hbm_frac_projection": round((cfg.V * cfg.d * 2) / (t_proj * 1e-6) / (HBM_PEAK_GBS * 1e9), 4),
+            "hbm_frac_library": round((cfg.V * cfg.d * 2) / (t_lib * 1e-6) / (HBM_PEAK_GBS * 1e9), 4)}), flush=True)
+        del call, prod, x, hidden, w_u, mask
+        torch.cuda.empty_cache()
+    return 0
+
+
 def proj_cost(cfg, rows: int):
     """Algorithmic HBM bytes and flops of one projection launch over ``rows``
     rows: W_U read once plus the rows, 2 flops per multiply-add."""
@@ -451,6 +503,9 @@ def main() -> int:
     ap.add_argument("--mfma-warmup", type=int, default=5)
     ap.add_argument("--mfma-cpu-positions", type=int, default=384,
                     help="masked positions of the oracle's sample for the mfma_regime CPU baseline")
+    ap.add_argument("--library-gemm", default=None, metavar="CONFIGS",
+                    help="calibration only: time the vendor library's bf16 GEMM (torch.mm) of the same rows "
+                         "beside the projection, for each comma-separated workload, and print one JSON line each")
     ap.add_argument("--event-every", type=int, default=4,
                     help="record the projection's HIP events on every N-th timed call (each event record "
                          "costs the stream a few microseconds)")
@@ -471,6 +526,8 @@ def main() -> int:
         from paper_2609_36452_amd.build import build
         build()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.library_gemm:
+        return bench_library_gemm(args, torch, rpd)
     cfg = CONFIGS[args.config]
     log(f"drawing workload {cfg.name} seed {args.seed}")
     t0 = time.perf_counter()
