@@ -329,7 +329,8 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
   // vocabulary rows 128*wv + 32*mv + 8*(q >> 2) + 4*(lane >> 5) + (q & 3)
   if (ve - vb == TV) {
     // A full vocabulary tile: no entry to exclude. Each projected row's 64
-    // raw accumulators in this lane take one max pass (3-input maxima); the
+    // raw accumulators in this lane take one max pass (3-input maxima that
+    // propagate NaN and need no canonicalized inputs); the
     // scale is positive, so the lowest slot holding the raw maximum is the
     // argmax of the scaled logits (slots increase with the vocabulary
     // index). The sums are taken in base-2 units: t = (z - m) log2(e) in one
@@ -343,9 +344,10 @@ __global__ __launch_bounds__(256) void k_proj_bf16_big(
 #pragma unroll
         for (int q = (mv == 0 ? 1 : 0); q < 16; q += 2) {
           if (q + 1 < 16)
-            mraw = __builtin_fmaxf(mraw, __builtin_fmaxf(acc[mv][nb][q], acc[mv][nb][q + 1]));
+            mraw = __builtin_elementwise_maximum(
+                mraw, __builtin_elementwise_maximum(acc[mv][nb][q], acc[mv][nb][q + 1]));
           else
-            mraw = __builtin_fmaxf(mraw, acc[mv][nb][q]);
+            mraw = __builtin_elementwise_maximum(mraw, acc[mv][nb][q]);
         }
       const float m2 = mraw * s2;
       int slot = 64;

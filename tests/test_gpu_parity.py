@@ -293,8 +293,9 @@ def test_exact_ties_take_the_lowest_index(name, ov, where):
     # An exact tie (gap 0 in exact arithmetic) is never excused by the comparator: duplicated rows must
     # give the lowest index at every layer, within a vocabulary tile ("near": copies 1-3 rows away, before
     # and after the target) and across tiles ("far": about V/2 away, in another tile and another XCD's
-    # range). The streaming kernel sums each tile in its own chunk order, so across its tiles the
-    # reduction resolves such ties; the eager and the lazy path (every position walking) are both checked.
+    # range). The streaming kernel sums each tile in its own chunk order and the MFMA tile with a single row
+    # tile one order per XCD, so across their tiles the reduction resolves such ties; the eager and the lazy
+    # path (every position walking) are both checked.
     cfg = CONFIGS["llada_late"].with_(name="dup_" + name, masked_frac=None, sharp=("calibrated", 0.0, 3.0),
                                       unstable_frac=0.3).with_(**ov)
     w = make_workload(cfg, 60)
