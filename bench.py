@@ -44,10 +44,39 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def code_tokens(src: str) -> str:
+    """C++ source without its comments, whitespace runs collapsed to one
+    space: what a counter measurement depends on (string and character
+    literals are kept whole)."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_sha(variant: str) -> str:
+    """Hash of the code (comments and layout excluded) of the files that
+    define a projection variant's kernel."""
     h = hashlib.sha256()
     for f in VARIANT_SOURCES[variant]:
-        h.update(open(os.path.join(CSRC, f), "rb").read())
+        h.update(code_tokens(open(os.path.join(CSRC, f), encoding="utf-8").read()).encode())
+        h.update(b"\0")
     return h.hexdigest()[:16]
 
 

@@ -55,7 +55,11 @@ namespace {
 // rows: 4% and 6% fewer main-loop cycles (9.5 ms at 12288 rows on one GPU);
 // the epilogue's sums in base-2 units from one fma per logit and 3-input
 // maxima: 0.2-1.6% less time from 192 to 12288 rows (interleaved A/B), the
-// 256-row form's spills down from 19 VGPRs to 3. Per tile at 12288 rows
+// 256-row form's spills down from 19 VGPRs to 3; the maxima on
+// NaN-propagating v_maximum3_f32 (fmaxf made the compiler canonicalize every
+// accumulator first): another 0.1-1.1%. The same tile on 16x16x32 MFMAs
+// (fragments of 16 rows x 32 k) measured 2-4% slower at 128-576 rows, and
+// its 256-row form spilled 338-538 VGPRs. Per tile at 12288 rows
 // (shader clock read at the phase boundaries): 9.5k cycles until the first
 // chunk has landed, 136.4k in the main loop (131k of MFMA issue), 15.4k in
 // the epilogue, 2k between tiles; the clock, read against the fixed 100 MHz

@@ -39,6 +39,15 @@ def test_every_variant_names_its_kernel_sources(variant):
     assert bench.VARIANT_KERNEL[variant].startswith("k_proj_")
 
 
+def test_source_hash_ignores_comments_and_layout_only():
+    a = 'int f(int x) {  // twice\n  return 2 * x; /* doubled */ }\nconst char* s = "// kept";\n'
+    b = 'int f(int x) {\n    return 2 * x;\n}\nconst char* s = "// kept";  // a new comment\n'
+    assert bench.code_tokens(a) == bench.code_tokens(b)
+    assert bench.code_tokens(a) != bench.code_tokens(a.replace("2 * x", "3 * x"))
+    assert bench.code_tokens(a) != bench.code_tokens(a.replace('"// kept"', '"// changed"'))
+    assert '"// kept"' in bench.code_tokens(a)
+
+
 def test_committed_traffic_summary_matches_the_kernel_source():
     # the benchmark's default workload runs the 32-row streaming variant; its committed counter summary
     # must have been taken on the kernel source as it is now, or the bench line reports no traffic
