@@ -185,8 +185,14 @@ typedef struct rpd_params {
  * Outputs, all device memory, shape [B][L] unless noted. Unmasked positions
  * receive: commit 0, token -1, persistence 0, flags 0 and 0.0f elsewhere.
  *   commit            1 if the position is in A_t (Section 3.2)
- *   token             y_i, the final-layer argmax (lowest index on ties),
- *                     for every masked position, committed or not
+ *   token             y_i, the final-layer argmax, for every masked
+ *                     position, committed or not. Ties go to the lowest
+ *                     index: logits equal in exact arithmetic are found
+ *                     exactly while |logit_scale| * sum_k |W_U[y,k] x_k|
+ *                     <= 256 (|max logit| + 1) at d = 4096 (the bound
+ *                     scales with 1/(d+1)); a positive gap below the fp32
+ *                     accumulation error 4 (d+1) 2^-24 sum_k |W_U[y,k] x_k|
+ *                     may go either way
  *   entropy           H(p_i^(K-1)) in nats (Eq. 1)
  *   confidence        c_i = p_i^(K-1)(y_i)
  *   persistence       K_i (Eq. 2), counted within the K supplied layers
