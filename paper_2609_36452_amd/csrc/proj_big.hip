@@ -67,7 +67,10 @@ namespace {
 // run, so the chip's power limit, not the schedule, sets most of the time.
 // A persistent form (one workgroup per CU looping over its tiles, the next
 // tile's W_U chunks loaded during the epilogue) spilled 110-140 VGPRs per
-// tile at 256 rows and measured 9-15% slower.
+// tile at 256 rows and measured 9-15% slower; rebuilt without spills at 128
+// and 192 rows, it was still 0-2% slower there and 6-10% slower from 256
+// rows up: workgroups walking fixed strides of jobs drift apart, where the
+// dispatcher's window of consecutive jobs keeps the L2 sharing intact.
 namespace big {
 constexpr int TV = kBigTileVocab, KC = 64;
 }  // namespace big
