@@ -9,8 +9,9 @@ tiles split across XCDs, and rows gathered through 32-bit buffer offsets or,
 from a hidden tensor of more than 2^31 bytes, 64-bit addresses). The
 full-size LLaDA-8B / Dream-7B shapes are compared at every masked position
 and layer too (whole sequences of the batched shapes), and additionally on
-sampled positions of the whole batches. Edge cases: exact argmax ties from
-duplicated unembedding rows, zero hidden rows (uniform distribution), empty
+sampled positions of the whole batches. Edge cases: vocabularies smaller
+than one tile (down to V = 1), exact argmax ties from duplicated unembedding
+rows, zero hidden rows (uniform distribution), empty
 sequences inside a batch, NaN rows, budget and window extremes."""
 import dataclasses
 import math
@@ -328,6 +329,36 @@ def test_zero_hidden_rows_give_the_uniform_distribution(name, ov):
     np.testing.assert_allclose(g["layer_conf"][:, m], 1.0 / V, rtol=1e-3)
     assert not (g["flags"][m] & rpd.FLAG_CANDIDATE).any()
     assert (g["n_commit"] == (w.mask.sum(1) > 0)).all()     # the fallback alone commits
+
+
+SMALL_V_CASES = [   # name (the projection variant), overrides; d = 264: four full 64-wide chunks and a tail
+    ("bf16_s32", dict(B=1, L=64, K=4, d=264, n_masked=8)),
+    ("bf16_big128", dict(B=1, L=64, K=4, d=264, n_masked=24)),
+    ("bf16_big", dict(B=1, L=80, K=4, d=264, n_masked=64)),
+]
+
+
+@pytest.mark.parametrize("name,ov", SMALL_V_CASES, ids=[c[0] for c in SMALL_V_CASES])
+@pytest.mark.parametrize("V", [1, 2, 255, 257])
+def test_vocabularies_smaller_than_a_tile(name, ov, V):
+    # fewer vocabulary rows than one 256-row tile (or just above it): one ragged tile for the MFMA forms, tiles
+    # of one or two rows for the streaming form. V = 1 is a point mass: H = 0, c = 1, argmax 0, so every
+    # masked position is a candidate through theta_h and, with zero entropy, every one commits.
+    cfg = CONFIGS["llada_late"].with_(name=f"smallV{V}_{name}", masked_frac=None, V=max(V, 2),
+                                      sharp=("calibrated", 0.0, 3.0), unstable_frac=0.3).with_(**ov)
+    w = make_workload(cfg, 70 + V)
+    if V == 1:
+        w.w_u = np.ascontiguousarray(w.w_u[:1])
+        w.cfg = w.cfg.with_(V=1)
+    variant = rpd.projection_variant(w.cfg.K, w.cfg.B, w.cfg.L, w.cfg.d, w.cfg.V, rpd.DTYPE_BF16,
+                                     max_masked=w.n_masked)
+    assert name == variant, (name, variant)
+    for P in (O.LLADA, O.strict(w.cfg.K, 1.0)):
+        g, o, _ = _check(w, P)
+        if V == 1:
+            m = w.mask != 0
+            assert (g["token"][m] == 0).all() and (g["entropy"][m] == 0.0).all() and (g["confidence"][m] == 1.0).all()
+            assert (g["commit"][m] == 1).all()
 
 
 def test_all_masked_and_single_layer():
