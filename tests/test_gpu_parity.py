@@ -335,6 +335,7 @@ SMALL_V_CASES = [   # name (the projection variant), overrides; d = 264: four fu
     ("bf16_s32", dict(B=1, L=64, K=4, d=264, n_masked=8)),
     ("bf16_big128", dict(B=1, L=64, K=4, d=264, n_masked=24)),
     ("bf16_big", dict(B=1, L=80, K=4, d=264, n_masked=64)),
+    ("f32", dict(B=1, L=64, K=3, d=72, n_masked=10, dtype="f32")),
 ]
 
 
@@ -350,7 +351,8 @@ def test_vocabularies_smaller_than_a_tile(name, ov, V):
     if V == 1:
         w.w_u = np.ascontiguousarray(w.w_u[:1])
         w.cfg = w.cfg.with_(V=1)
-    variant = rpd.projection_variant(w.cfg.K, w.cfg.B, w.cfg.L, w.cfg.d, w.cfg.V, rpd.DTYPE_BF16,
+    variant = rpd.projection_variant(w.cfg.K, w.cfg.B, w.cfg.L, w.cfg.d, w.cfg.V,
+                                     rpd.DTYPE_BF16 if w.cfg.dtype == "bf16" else rpd.DTYPE_F32,
                                      max_masked=w.n_masked)
     assert name == variant, (name, variant)
     for P in (O.LLADA, O.strict(w.cfg.K, 1.0)):
