@@ -363,6 +363,27 @@ def test_vocabularies_smaller_than_a_tile(name, ov, V):
             assert (g["commit"][m] == 1).all()
 
 
+MANY_LAYER_CASES = [   # name (the projection variant), overrides
+    ("bf16_s64", dict(B=1, L=40, K=64, d=136, V=3001, n_masked=1)),
+    ("bf16_big128", dict(B=1, L=40, K=13, d=136, V=3001, n_masked=8)),
+    ("bf16_big", dict(B=2, L=40, K=64, d=136, V=3001, n_masked=4)),
+]
+
+
+@pytest.mark.parametrize("name,ov", MANY_LAYER_CASES, ids=[c[0] + "_K%d" % c[1]["K"] for c in MANY_LAYER_CASES])
+def test_many_layers(name, ov):
+    # K = 13 (several layers per reduction wave, K above k_max = 6, so Eq. 4 caps the persistence) and
+    # K = 64 (the largest the boundary takes: one lane per layer in the stability evaluation), eager and
+    # with the lazy walk over every position
+    cfg = CONFIGS["llada_late"].with_(name=f"layers_{name}", masked_frac=None, sharp=("calibrated", 0.0, 4.0),
+                                      unstable_frac=0.3).with_(**ov)
+    w = make_workload(cfg, 90 + cfg.K)
+    variant = rpd.projection_variant(cfg.K, cfg.B, cfg.L, cfg.d, cfg.V, rpd.DTYPE_BF16, max_masked=w.n_masked)
+    assert name == variant, (name, variant)
+    for P in (O.LLADA, O.strict(cfg.K, 1.0), dataclasses.replace(O.LLADA, lazy=True, lazy_all=True)):
+        _check(w, P)
+
+
 def test_all_masked_and_single_layer():
     w = _small_bf16(n_masked=48)
     _check(w, O.LLADA)
