@@ -503,6 +503,26 @@ def test_gate_commit_matches_oracle_selection(block):
     assert (g["token"][~m] == -1).all() and (g["commit"][~m] == 0).all()
 
 
+def test_largest_canvas_the_boundary_takes():
+    # B * L = 2^24 positions (4096 sequences of 4096), the boundary's maximum, with 300 masked positions
+    # scattered over them: the compaction scans the whole canvas, the commitment runs one workgroup per
+    # sequence (most of them empty), and every masked position is compared with the oracle
+    from paper_2609_36452_amd.workload import Workload
+    B, L, K, d, V, n = 4096, 4096, 2, 8, 300, 300
+    assert B * L == 1 << 24
+    src = make_workload(CONFIGS["llada_late"].with_(name="max_canvas_rows", B=1, L=n, K=K, d=d, V=V, n_masked=n,
+                                                    masked_frac=None, sharp=("calibrated",), unstable_frac=0.3), 5)
+    flat = np.sort(np.random.default_rng(5).choice(B * L, size=n, replace=False))
+    hidden = np.zeros((K, B * L, d), np.uint16)
+    hidden[:, flat] = src.hidden[:, 0]
+    mask = np.zeros(B * L, np.uint8)
+    mask[flat] = 1
+    w = Workload(src.cfg.with_(name="max_canvas", B=B, L=L, n_masked=None), 5, src.w_u, hidden.reshape(K, B, L, d),
+                 mask.reshape(B, L), np.full((B, L), -1, np.int64))
+    g, o, _ = _check(w, O.LLADA)
+    assert int(g["n_commit"].sum()) == int((w.mask.sum(1) > 0).sum())   # one masked position each: one commit
+
+
 @pytest.mark.parametrize("n", [64, 72])
 def test_big_tile_wide_row_offsets(n):
     # With more than 2^31 bytes of hidden states the big tile gathers rows through 64-bit addresses
