@@ -28,6 +28,15 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
 RIDGE_ROWS = 315             # projected rows where the projection turns compute-bound
 
 METRIC = "masked positions scored+committed/sec at LLaDA-8B shape; MFMA % / HBM GB/s"
+# What the paper reports about the cost of this step, for context only (another GPU, whole decodes with
+# the backbone; nothing comparable to the step's own throughput here).
+PAPER_CONTEXT = {
+    "hardware": "one NVIDIA A6000, bf16, batch 1, 256-token canvas (Section 4.1)",
+    "commit_step_time": None,
+    "note": "the paper gives no absolute time for the projection, scoring and commitment; whole-decode "
+            "runtime relative to Fast-dLLM is 1.03x for RPD and 0.96x for RPD-block, the backbone forward "
+            "taking most of it (Section 4, decoding behavior and overhead, Figure 5c)",
+}
 CSRC = os.path.join(ROOT, "paper_2609_36452_amd", "csrc")
 # the source files that define each projection variant's kernel
 VARIANT_SOURCES = {v: ["rpd_device.h", "proj_stream.hip"] for v in
@@ -649,6 +658,7 @@ def main() -> int:
         out["cpu_baseline"] = cpu_baseline(w, OP, args.cpu_budget)
     if args.mfma_config and args.mfma_config != cfg.name and not args.norm and not args.lazy and not args.cold:
         out["mfma_regime"] = bench_mfma_regime(args, torch, rpd)
+    out["paper_context"] = PAPER_CONTEXT
     print(json.dumps(out), flush=True)
     return 0
 
